@@ -1,0 +1,126 @@
+"""Planted mistakes in the oracle (on the CPU) must be caught by its pins.
+
+Each case patches one plausible slip into the oracle -- a dropped term, a
+wrong scale, a swapped operand -- and checks that an independent reference
+no longer agrees.  Nothing here touches the GPU path.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import blob as oblob
+from oracle import dit, schedule
+from seeded_inputs import configs, generate
+from tests._torch_dit import torch_dit_eps
+
+CFG = configs.scaled(configs.TINY, name="tiny_cfg2", cfg_batch=2)
+
+
+@pytest.fixture(scope="module")
+def model():
+    hdr, params = oblob.read_blob(generate.make_weight_blob(CFG, 0))
+    x = generate.make_latent(CFG, 0).astype(np.float64)
+    return hdr, params, x, generate.make_labels(CFG, 0)
+
+
+def _full_eps_agrees(hdr, params, x, labels):
+    got = dit.denoiser_band(hdr, params, x, 0, CFG.R, 750, labels)["eps"]
+    ref = torch_dit_eps(hdr, params, x, 750, labels)
+    return np.allclose(got, ref, rtol=1e-9, atol=1e-10)
+
+
+MUTATIONS = {
+    "gelu_constant": ("gelu_tanh", lambda x: 0.5 * x * (1 + np.tanh(math.sqrt(2 / math.pi) * (x + 0.04 * x ** 3)))),
+    "gelu_exact_erf_like": ("gelu_tanh", lambda x: x / (1 + np.exp(-1.702 * x))),
+    "ln_unbiased_var": ("layer_norm", lambda h, eps=1e-6: (h - h.mean(-1, keepdims=True)) /
+                        np.sqrt(h.var(-1, ddof=1, keepdims=True) + eps)),
+    "ln_eps_1e-5": ("layer_norm", lambda h, eps=1e-6: (h - h.mean(-1, keepdims=True)) /
+                    np.sqrt(h.var(-1, keepdims=True) + 1e-2)),
+    "modulate_no_one": ("modulate", lambda u, shift, scale: u * scale + shift),
+    "sinusoid_sin_first": ("timestep_embedding", None),
+    "silu_as_sigmoid": ("silu", lambda x: 1 / (1 + np.exp(-x))),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_caught_by_torch_reference(model, monkeypatch, name):
+    hdr, params, x, labels = model
+    assert _full_eps_agrees(hdr, params, x, labels)
+    attr, fn = MUTATIONS[name]
+    orig = getattr(dit, attr)
+    if fn is None:          # [sin, cos] instead of [cos, sin]
+        def fn(t, dim=256, dtype=np.float64):
+            return np.roll(orig(t, dim, dtype), dim // 2)
+    monkeypatch.setattr(dit, attr, fn)
+    assert not _full_eps_agrees(hdr, params, x, labels)
+
+
+def test_mutation_attention_scale(model, monkeypatch):
+    hdr, params, x, labels = model
+    orig = dit.attention
+
+    def wrong(q, k, v, heads, q_chunk=2048):
+        d = q.shape[1] // heads
+        return orig(q / math.sqrt(d), k, v, heads, q_chunk)
+    monkeypatch.setattr(dit, "attention", wrong)
+    assert not _full_eps_agrees(hdr, params, x, labels)
+
+
+def test_mutation_patch_order(model, monkeypatch):
+    hdr, params, x, labels = model
+    orig = dit.patchify_rows
+
+    def wrong(hdr_, xf, rb, re):                 # (dy, dx, channel) instead of (channel, dy, dx)
+        v = orig(hdr_, xf, rb, re)
+        C, p = hdr_["in_ch"], hdr_["patch"]
+        return v.reshape(-1, C, p, p).transpose(0, 2, 3, 1).reshape(v.shape)
+    monkeypatch.setattr(dit, "patchify_rows", wrong)
+    assert not _full_eps_agrees(hdr, params, x, labels)
+
+
+@pytest.mark.parametrize("slip", ["offset_zero", "stale_band", "fresh_v_as_k"])
+def test_mutation_band_kv_caught_by_stitching(model, monkeypatch, slip):
+    """Slips in where the band's fresh K/V go break the stitching invariant
+    (stale buffer = the full step's own K/V => bands reproduce the full step)."""
+    hdr, params, x, labels = model
+    full = dit.full_step(hdr, params, x, 500, 250, labels, 1.5, keep_kv=True)
+    buf = dit.full_kv_buffer(hdr, full["kv"])
+    # perturb the buffer inside the band only: unused by a correct band step
+    R = hdr["grid"]
+    rb, re = 2, 5
+    noisy = buf.copy()
+    N, H = R * R, hdr["hidden"]
+    per = 2 * N * H
+    d = H // hdr["heads"]
+    for blk in range(hdr["n_blocks"] * 2):
+        for hh in range(hdr["heads"]):
+            s0 = blk * per + hh * N * d
+            noisy[s0 + rb * R * d:s0 + re * R * d] += 0.5
+    good = dit.patch_step(hdr, params, x, rb, re, 500, 250, labels, 1.5, noisy)
+    np.testing.assert_allclose(good["x_out"], full["x_out"][:, rb * 2:re * 2], rtol=1e-12, atol=1e-12)
+    orig = dit.assemble_kv
+
+    def wrong(stale, k, v, tok0):
+        if slip == "offset_zero":
+            return orig(stale, k, v, 0)
+        if slip == "stale_band":
+            return stale[0].copy(), stale[1].copy()
+        return orig(stale, v, v, tok0)
+    monkeypatch.setattr(dit, "assemble_kv", wrong)
+    bad = dit.patch_step(hdr, params, x, rb, re, 500, 250, labels, 1.5, noisy)
+    assert not np.allclose(bad["x_out"], full["x_out"][:, rb * 2:re * 2], rtol=1e-6, atol=1e-8)
+
+
+def test_mutation_scheduler_sign(monkeypatch):
+    """A sign slip in Bc breaks the forward-marginal invariant."""
+    ab = schedule.alpha_bar()
+    a_s, s_s = schedule.alpha_sigma(ab, 780)
+    a_p, s_p = schedule.alpha_sigma(ab, 760)
+    A, Bc, C = schedule.ddim_coefficients(ab, 780, 760)
+    x0, eps = 0.3, -1.25
+    x = a_s * x0 + s_s * eps
+    good = A * x - Bc * eps
+    bad = A * x + Bc * eps
+    assert abs(good - (a_p * x0 + s_p * eps)) < 1e-12
+    assert abs(bad - (a_p * x0 + s_p * eps)) > 1e-3
