@@ -1,0 +1,254 @@
+"""Benchmark: one device's patch-parallel DiT-XL/2 1024px denoising step.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--share 0.40]
+
+A step is one orch_patch_denoise_step call: the DiT-XL/2 denoiser (28 blocks,
+hidden 1152, 16 heads) on a band of token rows of the 64 x 64 token grid
+(40% = 26 rows = 1664 queries per branch), attention over all 4096 tokens
+(fresh K/V for the band, stale buffer for the rest, refreshed in place),
+classifier-free guidance batch 2, and the scheduler update, at the first
+post-warm-up step t 780 -> 760 of the 50-step schedule.  Inputs are seeded
+and synthetic (random N(0, 0.02) weights, N(0, 1) latent); the stale buffer
+is filled by one all-rows warm-up step at 800 -> 780.
+
+Prints one JSON line: algorithmic TFLOP/s of the step (value), ms per step,
+the per-kernel split with the dominant kernel's roofline, the share sweep,
+and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+METRIC = "patch-step ms and TFLOP/s vs bf16 MFMA peak, DiT-XL/2 1024px, 1 GPU"
+
+
+def step_flops(cfg, n_q: int) -> float:
+    """Algorithmic FLOPs of one band step (band tokens only; nothing for stale rows)."""
+    H, L, B, N = cfg.hidden, cfg.n_blocks, cfg.cfg_batch, cfg.n_kv
+    per_branch = n_q * (L * (24 * H * H + 4 * N * H) + 64 * H) + 12 * H * H * L + 4 * H * H
+    return float(B * per_branch + 512 * H + 2 * H * H)
+
+
+def _time_loop(torch, fn, iters: int, warm: int = 3) -> float:
+    """Average ms of fn() over `iters` launches, HIP events on the current stream."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(iters):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / iters
+
+
+def kernel_split(torch, L, cfg, n_q: int, iters: int):
+    """Per-kernel average launch time of the step's hot kernels at the
+    step's shapes, through the kernel-level entry points."""
+    dev = "cuda:0"
+    H, F, B, N, heads, d = cfg.hidden, cfg.mlp_hidden, cfg.cfg_batch, cfg.n_kv, cfg.heads, cfg.head_dim
+    M = B * n_q
+    bf = torch.bfloat16
+    g = torch.Generator(device=dev).manual_seed(0)
+
+    def rnd(*shape, dtype=bf, scale=1.0):
+        return (torch.randn(*shape, generator=g, device=dev) * scale).to(dtype)
+
+    u = rnd(M, H)
+    w_qkv, w_proj, w_fc1, w_fc2 = rnd(3 * H, H, scale=0.02), rnd(H, H, scale=0.02), \
+        rnd(F, H, scale=0.02), rnd(H, F, scale=0.02)
+    b3, b1, b4 = rnd(3 * H, dtype=torch.float32), rnd(H, dtype=torch.float32), rnd(F, dtype=torch.float32)
+    gate = rnd(B, H, dtype=torch.float32, scale=0.03)
+    h = rnd(M, H, dtype=torch.float32)
+    mlp = rnd(M, F)
+    q = rnd(B, heads, n_q, d)
+    kv = rnd(B * 2 * N * H, scale=0.7)
+    att = torch.empty(M, H, dtype=bf, device=dev)
+    mod = rnd(B, 3 * H, dtype=torch.float32, scale=0.1)
+    fl = {}
+    fl["qkv_gemm"] = (2.0 * M * H * 3 * H, lambda: L.qkv_projection(
+        u, B, n_q, H, w_qkv, b3, H, heads, q, kv, 2 * N * H, N, 0, 1))
+    fl["attention"] = (4.0 * B * n_q * N * H, lambda: L.attention(
+        q, kv, 2 * N * H, None, 0, 0, 0, B, heads, n_q, N, d, att, 1))
+    fl["proj_gemm"] = (2.0 * M * H * H, lambda: L.linear(att, M, H, w_proj, H, b1, 2, gate, H, n_q, h, 1))
+    fl["fc1_gemm"] = (2.0 * M * H * F, lambda: L.linear(u, M, H, w_fc1, F, b4, 1, None, 0, 1, mlp, 1))
+    fl["fc2_gemm"] = (2.0 * M * F * H, lambda: L.linear(mlp, M, F, w_fc2, H, b1, 2, gate, H, n_q, h, 1))
+    ln_bytes = 6.0 * M * H
+    fl["adaln_layernorm"] = (0.0, lambda: L.layernorm_modulate(h, M, H, n_q, mod, mod[:, H:], 3 * H, u, 1))
+    out = {}
+    for name, (flops, fn) in fl.items():
+        ms = _time_loop(torch, fn, iters)
+        rec = {"ms": round(ms, 5)}
+        if flops:
+            rec["tflops"] = round(flops / ms / 1e9, 1)
+            rec["flop_per_launch"] = flops
+        else:
+            rec["gbs"] = round(ln_bytes / ms / 1e6, 1)
+            rec["bytes_per_launch"] = ln_bytes
+        out[name] = rec
+    return out
+
+
+def cpu_baseline(cfg, blob, x, labels, stale, rb, re, t, tp, blocks: int):
+    """The oracle (float64 numpy) on the same band, truncated to `blocks`
+    DiT blocks; rate scaled to the metric's unit by the sample's FLOPs."""
+    import dataclasses
+
+    import numpy as np
+
+    from oracle import blob as oblob
+    from oracle import dit
+    hdr, params = oblob.read_blob(blob, np.float64)
+    hdr = dict(hdr, n_blocks=blocks)
+    t0 = time.perf_counter()
+    dit.patch_step(hdr, params, x, rb, re, t, tp, labels, cfg.cfg_scale, stale)
+    dt = time.perf_counter() - t0
+    small = dataclasses.replace(cfg, n_blocks=blocks)
+    fl = step_flops(small, (re - rb) * cfg.R)
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads") or 0) for i in threadpool_info()) or None
+    except Exception:
+        pass
+    if threads is None:
+        threads = len(os.sched_getaffinity(0))
+    return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{cfg.name} band rows [{rb},{re}), both guidance branches, first {blocks} of "
+                      f"{cfg.n_blocks} blocks, float64 numpy; {fl / 1e12:.3f} TFLOP in {dt:.1f} s",
+            "ms_per_full_step_extrapolated": round(step_flops(cfg, (re - rb) * cfg.R) / (fl / dt) * 1e3, 1)}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="dit_xl2_1024")
+    ap.add_argument("--share", type=float, default=0.40)
+    ap.add_argument("--kernel-iters", type=int, default=20)
+    ap.add_argument("--cpu-blocks", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    a = ap.parse_args(argv)
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {a.gpus}).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2509_04719_amd import _lib as L     # raises if liborch.so is missing
+    from paper_2509_04719_amd import schedule as psched
+    from seeded_inputs import configs, generate
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    dev = "cuda:0"
+    cfg = configs.get(a.config)
+    rows = psched.band_rows(a.share, cfg.R)
+    rb, re = 0, rows
+    n_q = cfg.n_q(rows)
+    t, tp = configs.headline_timestep_pair(cfg)
+    print(f"# bench {cfg.name}: band [{rb},{re}) of {cfg.R} rows, n_q {n_q}, t {t}->{tp}", flush=True)
+
+    blob = generate.make_weight_blob(cfg, 0)
+    ctx = L.DiTStep(cfg, blob)
+    x_np = generate.make_latent(cfg, 0)
+    labels = generate.make_labels(cfg, 0)
+    x = torch.from_numpy(x_np).to(dev)
+    kv = torch.empty(ctx.stale_kv_bytes() // 2, dtype=torch.bfloat16, device=dev)
+    p = cfg.patch
+    full_out = torch.empty((cfg.in_ch, cfg.latent, cfg.latent), device=dev)
+    # warm-up fill of the buffer: an all-rows step one grid interval earlier
+    ctx.step(x, 0, cfg.R, t + (t - tp), t, labels, cfg.cfg_scale, kv, 1, full_out)
+    out = torch.empty((cfg.in_ch, rows * p, cfg.latent), device=dev)
+
+    def one():
+        ctx.step(x, rb, re, t, tp, labels, cfg.cfg_scale, kv, 1, out)
+
+    for _ in range(a.warmup):
+        one()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
+    ev[0].record()
+    for i in range(a.steps):
+        one()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(a.steps)]
+    total_ms = ev[0].elapsed_time(ev[-1])
+    ms = total_ms / a.steps
+    flops = step_flops(cfg, n_q)
+    tflops = flops / ms / 1e9
+    print(f"# step {ms:.3f} ms (median {float(np.median(per)):.3f}), {tflops:.1f} TFLOP/s", flush=True)
+
+    split = kernel_split(torch, L, cfg, n_q, a.kernel_iters)
+    per_step = {k: v["ms"] * cfg.n_blocks for k, v in split.items()}
+    dom = max(per_step, key=per_step.get)
+    d = split[dom]
+    mfma_names = ["qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm"]
+    mfma_flops = sum(split[k]["flop_per_launch"] for k in mfma_names)
+    mfma_ms = sum(split[k]["ms"] for k in mfma_names)
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": d["tflops"], "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(d["tflops"] / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "flop_per_launch": d["flop_per_launch"], "ms_per_launch": d["ms"]}
+    print(f"# kernels: {json.dumps(split)}", flush=True)
+
+    sweep = {}
+    if not a.no_sweep:
+        for share in (0.10, 0.25, 0.40, 0.65, 1.00):
+            r = psched.band_rows(share, cfg.R)
+            o = torch.empty((cfg.in_ch, r * p, cfg.latent), device=dev)
+            m = _time_loop(torch, lambda: ctx.step(x, 0, r, t, tp, labels, cfg.cfg_scale, kv, 1, o), 10, 2)
+            sweep[f"{int(share * 100)}%"] = {"rows": r, "ms": round(m, 3),
+                                            "tflops": round(step_flops(cfg, cfg.n_q(r)) / m / 1e9, 1)}
+        print(f"# sweep: {json.dumps(sweep)}", flush=True)
+
+    cpu = None
+    if not a.no_cpu_baseline:
+        stale_host = kv.view(torch.int16).cpu().numpy().view(np.uint16)
+        cpu = cpu_baseline(cfg, blob, x_np, labels, stale_host, rb, re, t, tp, a.cpu_blocks)
+        print(f"# cpu baseline: {json.dumps(cpu)}", flush=True)
+
+    res = {
+        "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: DiT-XL/2 1024px band step, {rows}/{cfg.R} token rows "
+                               f"({a.share:.0%}), {n_q} queries x {cfg.n_kv} keys, CFG batch "
+                               f"{cfg.cfg_batch}, t {t}->{tp}, stale K/V refreshed",
+                   "global_batch": cfg.cfg_batch, "seq_len": n_q, "kv_len": cfg.n_kv,
+                   "parallelism": "none (one device's band)"},
+        "frac_of_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "step_ms_median": round(float(np.median(per)), 4),
+        "step_ms_p10_p90": [round(float(np.percentile(per, 10)), 4), round(float(np.percentile(per, 90)), 4)],
+        "attn_gemm_tflops": round(mfma_flops / mfma_ms / 1e9, 1),
+        "attn_gemm_frac": round(mfma_flops / mfma_ms / 1e9 / PEAK_BF16_TFLOPS, 4),
+        "roofline": roofline,
+        "kernels": split,
+        "share_sweep": sweep,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    ctx.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,194 @@
+/*
+ * orch.h -- C ABI of the MI355X (gfx950) patch-parallel DiT denoising step.
+ *
+ * One device's share of a patch-parallel denoising step (Algorithm 1: "one-step
+ * inference on p_i with buffer", then the buffer update; patch parallelism
+ * with stale activation reuse, §II-B): a DiT denoiser evaluated on an elastic
+ * band of latent token rows, whose attention reads the whole image's keys and
+ * values -- fresh for the band, stale from a buffer for every other row --
+ * followed by classifier-free guidance and the scheduler update of §I with the
+ * eps coefficient of Lemma 1 (Eq. (1)).
+ *
+ * Conventions for every entry point:
+ *   - Returns ORCH_OK (0) or a negative orch_status; orch_last_error() gives a
+ *     thread-local message for the last failure on the calling thread.
+ *   - Arguments are validated on the host before anything is launched: an
+ *     error return means nothing was written.
+ *   - Device pointers are HIP device addresses owned by the caller; the
+ *     library owns its weights and workspace.  Kernels are enqueued on
+ *     `hip_stream` (a hipStream_t; NULL = the default stream) and the call
+ *     returns without synchronising.  An asynchronous device fault surfaces as
+ *     ORCH_EHIP on a later call.
+ *   - A context is used by one host thread and one stream at a time.
+ *   - Element types: ORCH_F32 = IEEE float32; ORCH_BF16 = bfloat16 stored as
+ *     16-bit words.  Rounding to bf16 is round-to-nearest-even.
+ */
+#ifndef ORCH_H
+#define ORCH_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ORCH_OK = 0,
+  ORCH_EINVAL = -1,     /* bad argument, shape or blob                        */
+  ORCH_ENOWEIGHTS = -2, /* step called before orch_load_dit_weights            */
+  ORCH_EHIP = -3,       /* a HIP runtime call or kernel launch failed          */
+  ORCH_ENOMEM = -4      /* device allocation failed                            */
+} orch_status;
+
+enum { ORCH_F32 = 0, ORCH_BF16 = 1 };
+
+/* DiT shape and sampler constants.  hidden = heads * head_dim, head_dim in
+ * {32, 64, 72, 80, 96, 128}; hidden % 128 == 0; latent % patch == 0;
+ * patch == 2; cfg_batch in {1, 2}; T = number of DDPM steps of the
+ * linear-beta schedule beta = linspace(beta_start, beta_end, T). */
+typedef struct {
+  int n_blocks, hidden, heads, mlp_hidden;
+  int in_ch, out_ch, patch, latent;
+  int num_classes, freq_dim, cfg_batch, dtype;
+  int T;
+  double beta_start, beta_end;
+} orch_dit_config;
+
+typedef struct orch_ctx orch_ctx;
+
+/* Create a context on the current HIP device.  Allocates the workspace for a
+ * band of every row (so any band fits).  *out is set on success. */
+int orch_create(const orch_dit_config* cfg, orch_ctx** out);
+
+/* Release the context and its device memory.  NULL is ignored. */
+void orch_destroy(orch_ctx* ctx);
+
+/* Load the weight blob (host memory, `nbytes` bytes) and copy it to the
+ * device.  Blob format: 256-byte header (magic "ORCHDIT1", u32 version 1,
+ * u32 dtype, u32 n_blocks, hidden, heads, mlp_hidden, in_ch, out_ch, patch,
+ * grid, num_classes, freq_dim, n_tensors) followed by the tensors in the
+ * fixed DiT order, each 256-byte aligned, linear weights [out][in].  The
+ * header must match the context's config.  Synchronous. */
+int orch_load_dit_weights(orch_ctx* ctx, const void* host_blob, size_t nbytes);
+
+/* Bytes of the stale K/V buffer: n_blocks * cfg_batch * 2 * N_kv * hidden
+ * elements, N_kv = (latent/patch)^2.  Layout per (block l, branch b), at
+ * element offset (l * cfg_batch + b) * 2 * N_kv * hidden: K as
+ * [heads][N_kv][head_dim], then V transposed as [heads][head_dim][N_kv].
+ * Token index n = row * (latent/patch) + column. */
+size_t orch_stale_kv_bytes(const orch_ctx* ctx);
+
+/* One executed denoising step of one device (Algorithm 1; §I update with
+ * Lemma 1's coefficient).
+ *   x_full      device fp32 [in_ch][latent][latent]: the current sample x_t.
+ *   row_begin,  the band of token rows [row_begin, row_end),
+ *   row_end     0 <= row_begin < row_end <= latent/patch.
+ *   t, t_prev   source and target timesteps, 0 <= t < T, -1 <= t_prev < t;
+ *               t_prev = -1 means alpha_bar = 1 (the final step).
+ *   labels      host int[cfg_batch], each in [0, num_classes]; with guidance
+ *               labels[0] is the class and labels[1] the null label
+ *               (num_classes).
+ *   cfg_scale   guidance scale g: eps = eps_u + g (eps_c - eps_u); unused
+ *               when cfg_batch == 1.
+ *   stale_kv    device, orch_stale_kv_bytes() bytes in the config dtype.
+ *               Read for every token outside the band.  Not written unless
+ *               refresh != 0, and then only the band's tokens, which receive
+ *               this step's fresh K/V (Algorithm 1, buffer update).
+ *   z, eta      eta == 0: deterministic DDIM, z unused (may be NULL).
+ *               eta > 0: z device fp32 [in_ch][latent][latent] noise, added
+ *               with the eta-DDIM coefficient.
+ *   out_eps     device fp32 [cfg_batch][out_ch][2r][latent] or NULL: the
+ *               unguided eps of every branch for the band (r = row_end -
+ *               row_begin, 2r = r * patch latent rows).
+ *   out_x_patch device fp32 [in_ch][r*patch][latent]: the band of x_{t_prev}.
+ *               Must not overlap x_full, stale_kv or out_eps.
+ * Errors: ORCH_EINVAL for a bad band, timestep, label, NULL pointer or
+ * overlap; ORCH_ENOWEIGHTS before weights are loaded; ORCH_EHIP. */
+int orch_patch_denoise_step(orch_ctx* ctx, const float* x_full, int row_begin, int row_end,
+                            int t, int t_prev, const int* labels, float cfg_scale,
+                            void* stale_kv, int refresh, const float* z, float eta,
+                            float* out_eps, float* out_x_patch, void* hip_stream);
+
+/* The fused guidance + scheduler update of §I, elementwise over n floats:
+ *   eps = eps_uncond ? eps_uncond + g (eps_cond - eps_uncond) : eps_cond
+ *   out = a x - b eps + c z          (z may be NULL when c == 0)
+ * All pointers are device fp32 arrays of n elements; out may equal x. */
+int orch_scheduler_update(const float* x, const float* eps_cond, const float* eps_uncond,
+                          float cfg_scale, const float* z, double a, double b, double c,
+                          float* out, size_t n, void* hip_stream);
+
+/* Host only: coefficients (a, b, c) of the update for t -> t_prev under the
+ * config's schedule: alpha = sqrt(abar), sigma = sqrt(1 - abar),
+ * a = alpha_p / alpha_s, b = alpha_p sigma_s / alpha_s - sqrt(1 - abar_p - c^2)
+ * (Lemma 1's sigma_p (e^h - 1) when eta = 0), c = eta-DDIM noise scale. */
+int orch_schedule_coefficients(const orch_dit_config* cfg, int t, int t_prev, double eta,
+                               double out_abc[3]);
+
+/* Thread-local message describing the last error ("" if none). */
+const char* orch_last_error(void);
+
+/* ---- kernel-level entry points ------------------------------------------
+ * The kernels of the step, callable one at a time on caller buffers (same
+ * launch configuration the step uses).  `dtype` is ORCH_F32 or ORCH_BF16 and
+ * applies to every non-fp32 operand named "T" below. */
+
+/* adaLN LayerNorm: out[m][:] = LN(x[m][:]) * (1 + scale[b][:]) + shift[b][:],
+ * b = m / rows_per_batch; LN over `hidden` without affine, eps 1e-6, biased
+ * variance, fp32 statistics.  x fp32 [rows][hidden]; shift, scale fp32 rows
+ * of a [B][mod_stride] array; out T [rows][hidden]. */
+int orch_op_layernorm_modulate(const float* x, int rows, int hidden, int rows_per_batch,
+                               const float* shift, const float* scale, int mod_stride,
+                               void* out, int dtype, void* hip_stream);
+
+enum { ORCH_EPI_STORE = 0, ORCH_EPI_GELU = 1, ORCH_EPI_RESIDUAL = 2 };
+
+/* y = A W^T + bias with A T [M][K], W T [N][K], bias fp32 [N], fp32
+ * accumulation.  epilogue STORE: out T [M][N] = y.  GELU: out T = GELU_tanh(y).
+ * RESIDUAL: out fp32 [M][N] += gate[b][n] * y, gate fp32 rows of a
+ * [B][gate_stride] array, b = m / rows_per_batch. */
+int orch_op_linear(const void* A, int M, int K, const void* W, int N, const float* bias,
+                   int epilogue, const float* gate, int gate_stride, int rows_per_batch,
+                   void* out, int dtype, void* hip_stream);
+
+/* The QKV projection with its scatter epilogue.  A T [B*n_tok][K], W T
+ * [3H][K], bias fp32 [3H].  Q goes to q_out T [B][heads][n_tok][d]; K and V
+ * of token i of branch b go to kv_out + b * kv_branch_stride, K at
+ * [heads][kv_tokens][d] and V at offset kv_tokens*H as [heads][d][kv_tokens],
+ * both at token index tok_offset + i. */
+int orch_op_qkv_projection(const void* A, int B, int n_tok, int K, const void* W,
+                           const float* bias, int hidden, int heads, void* q_out,
+                           void* kv_out, size_t kv_branch_stride, int kv_tokens, int tok_offset,
+                           int dtype, void* hip_stream);
+
+/* Attention of a band's queries over the whole image (§II-B, stale K/V):
+ * for branch b, head j: O = softmax(Q K^T / sqrt(d)) V.  q T [B][heads][n_q][d].
+ * Keys/values of token n come from `kv_fresh` when fresh_begin <= n <
+ * fresh_begin + n_fresh (fresh token n - fresh_begin; K [heads][n_fresh][d],
+ * V at offset n_fresh*H as [heads][d][n_fresh], branch stride
+ * fresh_branch_stride) and from `kv_stale` otherwise (buffer layout, branch
+ * stride stale_branch_stride).  n_fresh may be 0.  out T [B][n_q][H]. */
+int orch_op_attention(const void* q, const void* kv_stale, size_t stale_branch_stride,
+                      const void* kv_fresh, size_t fresh_branch_stride, int fresh_begin,
+                      int n_fresh, int B, int heads, int n_q, int n_kv, int head_dim, void* out,
+                      int dtype, void* hip_stream);
+
+/* Conditioning of the loaded model: out fp32 [cfg_batch][6*H*n_blocks + 2*H],
+ * the adaLN vectors of every block followed by the final layer's
+ * (shift, scale), for timestep t and host labels[cfg_batch]. */
+int orch_op_conditioning(orch_ctx* ctx, int t, const int* labels, float* out, void* hip_stream);
+
+/* Patch embedding of the band's tokens plus the position table:
+ * out fp32 [cfg_batch][r*R][H] (identical rows for every branch). */
+int orch_op_patch_embed(orch_ctx* ctx, const float* x_full, int row_begin, int row_end,
+                        float* out, void* hip_stream);
+
+/* Final layer of the loaded model on h fp32 [cfg_batch][r*R][H] with the
+ * final (shift, scale) of `mod` (the conditioning output): out_eps fp32
+ * [cfg_batch][out_ch][r*patch][latent]. */
+int orch_op_final_layer(orch_ctx* ctx, const float* h, int row_begin, int row_end,
+                        const float* mod, float* out_eps, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ORCH_H */

@@ -1,0 +1,190 @@
+"""ctypes binding of liborch.so (argument marshalling only).
+
+Every function here forwards to the C ABI declared in include/orch.h; all
+computation happens in the library's HIP kernels.  PyTorch is used only to
+hold device memory and to name the current HIP stream.  Importing this
+module raises if the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liborch.so")
+
+ORCH_OK, ORCH_EINVAL, ORCH_ENOWEIGHTS, ORCH_EHIP, ORCH_ENOMEM = 0, -1, -2, -3, -4
+ORCH_F32, ORCH_BF16 = 0, 1
+EPI_STORE, EPI_GELU, EPI_RESIDUAL = 0, 1, 2
+DTYPE_CODE = {"f32": ORCH_F32, "bf16": ORCH_BF16}
+
+SYMBOLS = (
+    "orch_create", "orch_destroy", "orch_load_dit_weights", "orch_stale_kv_bytes",
+    "orch_patch_denoise_step", "orch_scheduler_update", "orch_schedule_coefficients",
+    "orch_last_error", "orch_op_layernorm_modulate", "orch_op_linear", "orch_op_qkv_projection",
+    "orch_op_attention", "orch_op_conditioning", "orch_op_patch_embed", "orch_op_final_layer",
+)
+
+
+class OrchError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"orch error {code}: {msg}")
+        self.code = code
+
+
+class OrchConfig(C.Structure):
+    _fields_ = [("n_blocks", C.c_int), ("hidden", C.c_int), ("heads", C.c_int),
+                ("mlp_hidden", C.c_int), ("in_ch", C.c_int), ("out_ch", C.c_int),
+                ("patch", C.c_int), ("latent", C.c_int), ("num_classes", C.c_int),
+                ("freq_dim", C.c_int), ("cfg_batch", C.c_int), ("dtype", C.c_int),
+                ("T", C.c_int), ("beta_start", C.c_double), ("beta_end", C.c_double)]
+
+
+def config_from(cfg) -> OrchConfig:
+    """Build the C config from any object with the DiT shape attributes."""
+    return OrchConfig(cfg.n_blocks, cfg.hidden, cfg.heads, cfg.mlp_hidden, cfg.in_ch, cfg.out_ch,
+                      cfg.patch, cfg.latent, cfg.num_classes, cfg.freq_dim, cfg.cfg_batch,
+                      DTYPE_CODE[cfg.dtype], cfg.T, cfg.beta_start, cfg.beta_end)
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2509_04719_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    vp, i, sz, d, f = C.c_void_p, C.c_int, C.c_size_t, C.c_double, C.c_float
+    sig = {
+        "orch_create": (i, [C.POINTER(OrchConfig), C.POINTER(vp)]),
+        "orch_destroy": (None, [vp]),
+        "orch_load_dit_weights": (i, [vp, vp, sz]),
+        "orch_stale_kv_bytes": (sz, [vp]),
+        "orch_patch_denoise_step": (i, [vp, vp, i, i, i, i, C.POINTER(i), f, vp, i, vp, f, vp, vp,
+                                        vp]),
+        "orch_scheduler_update": (i, [vp, vp, vp, f, vp, d, d, d, vp, sz, vp]),
+        "orch_schedule_coefficients": (i, [C.POINTER(OrchConfig), i, i, d, C.POINTER(d)]),
+        "orch_last_error": (C.c_char_p, []),
+        "orch_op_layernorm_modulate": (i, [vp, i, i, i, vp, vp, i, vp, i, vp]),
+        "orch_op_linear": (i, [vp, i, i, vp, i, vp, i, vp, i, i, vp, i, vp]),
+        "orch_op_qkv_projection": (i, [vp, i, i, i, vp, vp, i, i, vp, vp, sz, i, i, i, vp]),
+        "orch_op_attention": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, i, vp]),
+        "orch_op_conditioning": (i, [vp, i, C.POINTER(i), vp, vp]),
+        "orch_op_patch_embed": (i, [vp, vp, i, i, vp, vp]),
+        "orch_op_final_layer": (i, [vp, vp, i, i, vp, vp, vp]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+def last_error() -> str:
+    return lib.orch_last_error().decode()
+
+
+def check(rc: int) -> None:
+    if rc != ORCH_OK:
+        raise OrchError(rc, last_error())
+
+
+def _ptr(t):
+    """Device address of a torch tensor (or None)."""
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def schedule_coefficients(cfg, t: int, t_prev: int, eta: float = 0.0):
+    """(a, b, c) of x_prev = a x - b eps + c z, computed by the library (host)."""
+    out = (C.c_double * 3)()
+    oc = config_from(cfg)
+    check(lib.orch_schedule_coefficients(C.byref(oc), t, t_prev, eta, out))
+    return out[0], out[1], out[2]
+
+
+class DiTStep:
+    """A library context for one DiT config: weights + workspace on the GPU."""
+
+    def __init__(self, cfg, blob=None):
+        self.cfg = cfg
+        self._c = config_from(cfg)
+        h = C.c_void_p()
+        check(lib.orch_create(C.byref(self._c), C.byref(h)))
+        self.handle = h
+        if blob is not None:
+            self.load(blob)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib.orch_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        self.close()
+
+    def load(self, blob):
+        import numpy as np
+        b = np.ascontiguousarray(blob, dtype=np.uint8)
+        check(lib.orch_load_dit_weights(self.handle, b.ctypes.data_as(C.c_void_p), b.nbytes))
+
+    def stale_kv_bytes(self) -> int:
+        return lib.orch_stale_kv_bytes(self.handle)
+
+    def step(self, x_full, row_begin, row_end, t, t_prev, labels, cfg_scale, stale_kv,
+             refresh, out_x, out_eps=None, z=None, eta=0.0, stream=None):
+        lab = (C.c_int * len(labels))(*[int(v) for v in labels])
+        check(lib.orch_patch_denoise_step(self.handle, _ptr(x_full), row_begin, row_end, t, t_prev,
+                                          lab, float(cfg_scale), _ptr(stale_kv), int(refresh),
+                                          _ptr(z), float(eta), _ptr(out_eps), _ptr(out_x),
+                                          _stream(stream)))
+
+    def conditioning(self, t, labels, out, stream=None):
+        lab = (C.c_int * len(labels))(*[int(v) for v in labels])
+        check(lib.orch_op_conditioning(self.handle, t, lab, _ptr(out), _stream(stream)))
+
+    def patch_embed(self, x_full, row_begin, row_end, out, stream=None):
+        check(lib.orch_op_patch_embed(self.handle, _ptr(x_full), row_begin, row_end, _ptr(out),
+                                      _stream(stream)))
+
+    def final_layer(self, h, row_begin, row_end, mod, out_eps, stream=None):
+        check(lib.orch_op_final_layer(self.handle, _ptr(h), row_begin, row_end, _ptr(mod),
+                                      _ptr(out_eps), _stream(stream)))
+
+
+def scheduler_update(x, eps_cond, eps_uncond, cfg_scale, z, a, b, c, out, stream=None):
+    check(lib.orch_scheduler_update(_ptr(x), _ptr(eps_cond), _ptr(eps_uncond), float(cfg_scale),
+                                    _ptr(z), a, b, c, _ptr(out), out.numel(), _stream(stream)))
+
+
+def layernorm_modulate(x, rows, hidden, rows_per_batch, shift, scale, mod_stride, out, dtype,
+                       stream=None):
+    check(lib.orch_op_layernorm_modulate(_ptr(x), rows, hidden, rows_per_batch, _ptr(shift),
+                                         _ptr(scale), mod_stride, _ptr(out), dtype,
+                                         _stream(stream)))
+
+
+def linear(A, M, K, W, N, bias, epilogue, gate, gate_stride, rows_per_batch, out, dtype,
+           stream=None):
+    check(lib.orch_op_linear(_ptr(A), M, K, _ptr(W), N, _ptr(bias), epilogue, _ptr(gate),
+                             gate_stride, rows_per_batch, _ptr(out), dtype, _stream(stream)))
+
+
+def qkv_projection(A, B, n_tok, K, W, bias, hidden, heads, q_out, kv_out, kv_branch_stride,
+                   kv_tokens, tok_offset, dtype, stream=None):
+    check(lib.orch_op_qkv_projection(_ptr(A), B, n_tok, K, _ptr(W), _ptr(bias), hidden, heads,
+                                     _ptr(q_out), _ptr(kv_out), kv_branch_stride, kv_tokens,
+                                     tok_offset, dtype, _stream(stream)))
+
+
+def attention(q, kv_stale, stale_bs, kv_fresh, fresh_bs, fresh_begin, n_fresh, B, heads, n_q,
+              n_kv, head_dim, out, dtype, stream=None):
+    check(lib.orch_op_attention(_ptr(q), _ptr(kv_stale), stale_bs, _ptr(kv_fresh), fresh_bs,
+                                fresh_begin, n_fresh, B, heads, n_q, n_kv, head_dim, _ptr(out),
+                                dtype, _stream(stream)))

@@ -1,0 +1,95 @@
+// Internal launchers of the gfx950 kernels.  All take device pointers and
+// enqueue on `stream`; they return the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+namespace orch {
+
+enum Dtype { kF32 = 0, kBF16 = 1 };
+enum Epi { kEpiStore = 0, kEpiGelu = 1, kEpiResidual = 2, kEpiQkv = 3 };
+
+// Epilogue parameters of the projection GEMMs.
+struct EpiParams {
+  void* out;                  // STORE / GELU: T [M][N]; RESIDUAL: fp32 [M][N]
+  const float* bias;          // fp32 [N]
+  const float* gate;          // RESIDUAL: fp32 [B][gate_stride]
+  int gate_stride;
+  int rows_per_batch;         // rows of one guidance branch
+  // QKV scatter
+  void* q;                    // T [B][heads][n_tok][d]
+  void* kv;                   // T, branch b at kv + b*kv_branch_stride
+  size_t kv_branch_stride;    // elements
+  int kv_tokens;              // token extent of the K/V destination
+  int tok_offset;             // destination token of the first row
+  int heads, hidden, head_dim;
+};
+
+// y = A W^T (+ epilogue).  A T [M][K], W T [N][K].
+hipError_t launch_gemm(const void* A, const void* W, int M, int N, int K, int epi,
+                       const EpiParams& ep, int dtype, hipStream_t stream);
+
+// True when the MFMA GEMM handles this shape (bf16, N % 128 == 0, K % 64 == 0).
+bool gemm_uses_mfma(int N, int K, int dtype);
+
+hipError_t launch_layernorm_modulate(const float* x, int rows, int hidden, int rows_per_batch,
+                                     const float* shift, const float* scale, int mod_stride,
+                                     void* out, int dtype, hipStream_t stream);
+
+struct AttnParams {
+  const void* q;              // T [B][heads][n_q][d]
+  const void* kv_stale;       // T buffer layout, branch stride stale_bs
+  size_t stale_bs;
+  const void* kv_fresh;       // T, branch stride fresh_bs; may be null when n_fresh == 0
+  size_t fresh_bs;
+  int fresh_begin, n_fresh;
+  int B, heads, n_q, n_kv, d;
+  void* out;                  // T [B][n_q][heads*d]
+};
+
+hipError_t launch_attention(const AttnParams& p, int dtype, hipStream_t stream);
+bool attention_uses_mfma(int d, int n_kv, int dtype);
+
+// Conditioning.  temb: fp32 [H] scratch; sc: fp32 [B][H] SiLU(c);
+// mod: fp32 [B][n_mod].
+struct CondParams {
+  const void* w_t1; const float* b_t1;     // [H][freq], [H]
+  const void* w_t2; const float* b_t2;     // [H][H], [H]
+  const void* table;                        // [(classes+1)][H]
+  const void* w_ada; const float* b_ada;   // [n_mod][H], [n_mod]
+  int hidden, freq_dim, n_mod, B;
+  int labels[2];
+  float t;
+  float* t1;                                // fp32 [H] scratch
+  float* sc;                                // fp32 [B][H]
+  float* mod;                               // fp32 [B][n_mod]
+};
+hipError_t launch_conditioning(const CondParams& p, int dtype, hipStream_t stream);
+
+struct PatchEmbedParams {
+  const float* x;        // fp32 [C][latent][latent]
+  const float* w;        // fp32 [H][C*p*p]
+  const float* b;        // fp32 [H]
+  const float* pos;      // fp32 [N_kv][H]
+  float* h;              // fp32 [B][n_tok][H]
+  int C, latent, patch, grid, hidden, row_begin, n_rows, B;
+};
+hipError_t launch_patch_embed(const PatchEmbedParams& p, hipStream_t stream);
+
+struct FinalParams {
+  const void* u;         // T [B][n_tok][H] (already LN-modulated)
+  const void* w;         // T [p*p*Co][H]
+  const float* b;        // fp32 [p*p*Co]
+  float* eps;            // fp32 [B][Co][n_rows*p][latent]
+  int B, n_tok, hidden, out_ch, patch, grid, n_rows;
+};
+hipError_t launch_final_linear(const FinalParams& p, int dtype, hipStream_t stream);
+
+// out = a x - b (eu + g (ec - eu)) + c z over a [rows][cols] region; x has
+// row stride ldx, z row stride ldz, the rest row stride cols.  eu, z nullable.
+hipError_t launch_update(const float* x, int ldx, const float* ec, const float* eu, float g,
+                         const float* z, int ldz, float a, float b, float c, float* out, int rows,
+                         size_t cols, hipStream_t stream);
+
+}  // namespace orch

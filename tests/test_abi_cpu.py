@@ -1,0 +1,79 @@
+"""The C ABI library loads, exports every declared entry point, and its
+host-side logic (scheduler coefficients, step schedules) agrees with the
+oracle.  No device work: runs without a GPU."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import schedule as osched
+from paper_2509_04719_amd import schedule as psched
+from seeded_inputs import configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "orch.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(orch_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_expected_symbols(orch_lib):
+    assert _declared_functions() == sorted(orch_lib.SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(orch_lib):
+    names = _declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(orch_lib.lib, n), n
+    out = os.popen(f"nm -D --defined-only {orch_lib.LIB_PATH}").read()
+    exported = set(re.findall(r"\bT (orch_\w+)", out))
+    assert set(names) <= exported
+
+
+@pytest.mark.parametrize("pair", osched.step_pairs(1000, 50) + osched.step_pairs(1000, 4)
+                         + [(780, 740), (40, -1), (999, 998)])
+@pytest.mark.parametrize("eta", [0.0, 0.5, 1.0])
+def test_library_schedule_coefficients_match_oracle(orch_lib, pair, eta):
+    t, tp = pair
+    a, b, c = orch_lib.schedule_coefficients(configs.DIT_XL2_1024, t, tp, eta)
+    A, B, Cc = osched.ddim_coefficients(osched.alpha_bar(), t, tp, eta)
+    assert a == pytest.approx(A, rel=1e-12)
+    assert b == pytest.approx(B, rel=1e-10, abs=1e-14)
+    assert c == pytest.approx(Cc, rel=1e-10, abs=1e-14)
+
+
+@pytest.mark.parametrize("t,tp", [(1000, 500), (-1, -1), (500, 500), (500, 600), (10, -2)])
+def test_library_schedule_rejects_bad_pairs(orch_lib, t, tp):
+    with pytest.raises(orch_lib.OrchError) as e:
+        orch_lib.schedule_coefficients(configs.TINY, t, tp)
+    assert e.value.code == orch_lib.ORCH_EINVAL
+    assert "t_prev" in orch_lib.last_error()
+
+
+def test_product_schedules_match_oracle():
+    for M in (4, 20, 50):
+        ps = psched.plain_schedule(1000, M)
+        assert [(s.t, s.t_prev) for s in ps] == osched.step_pairs(1000, M)
+    ts = psched.tiered_schedule(1000, 50, 10)
+    assert [(s.m, s.t, s.t_prev, s.refresh) for s in ts] == osched.tiered_schedule(1000, 50, 10)
+    assert len(ts) == 30
+
+
+def test_band_rows_rounding():
+    assert [psched.band_rows(s, 64) for s in (0.10, 0.25, 0.40, 0.65, 1.0)] == [6, 16, 26, 42, 64]
+    assert [psched.band_rows(s, 128) for s in (1 / 8, 3 / 8, 5 / 8)] == [16, 48, 80]
+    assert psched.band_rows(0.40, 16) == 6
+    assert configs.DIT_XL2_1024.band_rows == (6, 16, 26, 42, 64)
+
+
+def test_create_rejects_bad_config_without_gpu_work(orch_lib):
+    import ctypes as C
+    bad = orch_lib.config_from(configs.scaled(configs.TINY, heads=3))
+    h = C.c_void_p()
+    rc = orch_lib.lib.orch_create(C.byref(bad), C.byref(h))
+    assert rc == orch_lib.ORCH_EINVAL and not h.value
+    assert "heads" in orch_lib.last_error()

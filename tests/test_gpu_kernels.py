@@ -1,0 +1,274 @@
+"""Kernel-level parity of the HIP path against the oracle, through the C ABI.
+
+Each kernel runs on seeded inputs at shapes that span several tiles with a
+ragged tail, and at the full DiT-XL/2 1024px (40% band) shape in the launch
+configuration of the step, where the oracle checks sampled rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import blob as oblob
+from oracle import dit, schedule as osched
+from seeded_inputs import configs, generate
+from tests._gpu_util import (DEV, bits_to_dev, code, empty, rel_l2, rounded, to_dev, to_host)
+
+pytestmark = pytest.mark.gpu
+
+XL = configs.DIT_XL2_1024
+XL_M = XL.cfg_batch * XL.n_q(26)      # 3328 rows: the 40% band, both branches
+
+
+# ---- adaLN LayerNorm ------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("rows,H,rpb", [(1, 128, 1), (97, 384, 50), (3328, 1152, 1664)])
+def test_layernorm_modulate(orch_lib, dtype, rows, H, rpb):
+    rng = np.random.default_rng(rows + H)
+    x = rng.standard_normal((rows, H)) * 2.0 + 0.5
+    B = (rows + rpb - 1) // rpb
+    mod = rng.standard_normal((B, 3 * H)) * 0.1
+    shift, scale = mod[:, H:2 * H], mod[:, 2 * H:]
+    xd, md = to_dev(x), to_dev(mod)
+    out = empty((rows, H), dtype)
+    orch_lib.layernorm_modulate(xd, rows, H, rpb, md[:, H:], md[:, 2 * H:], 3 * H, out, code(dtype))
+    xr, mr = rounded(x, "f32"), rounded(mod, "f32")
+    b = np.arange(rows) // rpb
+    ref = dit.modulate(dit.layer_norm(xr), mr[b, H:2 * H], mr[b, 2 * H:])
+    err = rel_l2(to_host(out), ref)
+    assert err <= (1e-6 if dtype == "f32" else 4e-3), err
+
+
+# ---- projection GEMMs -------------------------------------------------------
+
+GEMM_SHAPES = [(1, 128, 128), (96, 384, 1152), (200, 1536, 384), (333, 1152, 3456)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("M,K,N", GEMM_SHAPES)
+@pytest.mark.parametrize("epi", [0, 1, 2])
+def test_linear(orch_lib, dtype, M, K, N, epi):
+    rng = np.random.default_rng(M * 7 + K + N + epi)
+    A = rng.standard_normal((M, K))
+    W = rng.standard_normal((N, K)) * 0.02
+    bias = rng.standard_normal(N) * 0.02
+    Ar, Wr, br = rounded(A, dtype), rounded(W, dtype), rounded(bias, "f32")
+    y = dit.linear(Ar, Wr, br)
+    Ad, Wd, bd = to_dev(A, dtype), to_dev(W, dtype), to_dev(bias)
+    if epi == 2:
+        rpb = max(1, M // 2)
+        nb = (M + rpb - 1) // rpb
+        gate = rng.standard_normal((nb, N + 16)) * 0.5
+        h0 = rng.standard_normal((M, N))
+        gd, out = to_dev(gate), to_dev(h0)
+        orch_lib.linear(Ad, M, K, Wd, N, bd, 2, gd, N + 16, rpb, out, code(dtype))
+        g = rounded(gate, "f32")[np.arange(M) // rpb, :N]
+        got = to_host(out) - rounded(h0, "f32")
+        err = rel_l2(got, g * y)
+        assert err <= 2e-5, err
+    else:
+        out = empty((M, N), dtype)
+        orch_lib.linear(Ad, M, K, Wd, N, bd, epi, None, 0, 1, out, code(dtype))
+        ref = dit.gelu_tanh(y) if epi == 1 else y
+        err = rel_l2(to_host(out), ref)
+        assert err <= (1e-5 if dtype == "f32" else 5e-3), err
+
+
+@pytest.mark.parametrize("K,N,epi", [(1152, 3456, 0), (1152, 1152, 2), (1152, 4608, 1), (4608, 1152, 2)])
+def test_linear_full_xl_shape_sampled(orch_lib, K, N, epi):
+    """The four projections of DiT-XL/2 at the 40% band (M = 3328), sampled rows."""
+    M = XL_M
+    rng = np.random.default_rng(K + N)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    bias = (rng.standard_normal(N) * 0.02).astype(np.float32)
+    Ad, Wd, bd = to_dev(A, "bf16"), to_dev(W, "bf16"), to_dev(bias)
+    rows = np.sort(rng.choice(M, 48, replace=False))
+    rows[-1] = M - 1
+    Ar, Wr = rounded(A[rows], "bf16"), rounded(W, "bf16")
+    y = dit.linear(Ar, Wr, bias.astype(np.float64))
+    if epi == 2:
+        gate = (rng.standard_normal((2, N)) * 0.5).astype(np.float32)
+        h0 = np.zeros((M, N), np.float32)
+        out = to_dev(h0)
+        orch_lib.linear(Ad, M, K, Wd, N, bd, 2, to_dev(gate), N, M // 2, out, 1)
+        ref = gate.astype(np.float64)[rows // (M // 2)] * y
+        err = rel_l2(to_host(out)[rows], ref)
+        assert err <= 2e-5, err
+    else:
+        out = empty((M, N), "bf16")
+        orch_lib.linear(Ad, M, K, Wd, N, bd, epi, None, 0, 1, out, 1)
+        ref = dit.gelu_tanh(y) if epi == 1 else y
+        err = rel_l2(to_host(out)[rows], ref)
+        assert err <= 5e-3, err
+
+
+# ---- QKV projection with the buffer scatter ---------------------------------
+
+@pytest.mark.parametrize("dtype,H,heads,n_tok,kv_tokens,off", [
+    ("f32", 128, 4, 32, 64, 16), ("bf16", 384, 6, 96, 256, 96), ("bf16", 1152, 16, 384, 1024, 640)])
+def test_qkv_scatter(orch_lib, dtype, H, heads, n_tok, kv_tokens, off):
+    B = 2
+    d = H // heads
+    rng = np.random.default_rng(H)
+    A = rng.standard_normal((B * n_tok, H))
+    W = rng.standard_normal((3 * H, H)) * 0.02
+    bias = rng.standard_normal(3 * H) * 0.02
+    y = dit.linear(rounded(A, dtype), rounded(W, dtype), rounded(bias, "f32"))
+    stride = 2 * kv_tokens * H + 64
+    canary = rng.standard_normal(B * stride)
+    kv = to_dev(canary, dtype)
+    q = empty((B, heads, n_tok, d), dtype)
+    orch_lib.qkv_projection(to_dev(A, dtype), B, n_tok, H, to_dev(W, dtype), to_dev(bias), H, heads,
+                            q, kv, stride, kv_tokens, off, code(dtype))
+    tol = 1e-5 if dtype == "f32" else 5e-3
+    qh = to_host(q)
+    kvh = to_host(kv).reshape(B, stride)
+    can = rounded(canary, dtype).reshape(B, stride)
+    hdr = {"hidden": H, "heads": heads, "grid": int(np.sqrt(kv_tokens))}
+    for b in range(B):
+        yb = y[b * n_tok:(b + 1) * n_tok]
+        qref = yb[:, :H].reshape(n_tok, heads, d).transpose(1, 0, 2)
+        assert rel_l2(qh[b], qref) <= tol
+        K, V = dit.stale_kv_block(hdr, kvh[b, :2 * kv_tokens * H], 1, 0, 0)
+        K0, V0 = dit.stale_kv_block(hdr, can[b, :2 * kv_tokens * H], 1, 0, 0)
+        band = slice(off, off + n_tok)
+        assert rel_l2(K[band], yb[:, H:2 * H]) <= tol
+        assert rel_l2(V[band], yb[:, 2 * H:]) <= tol
+        # every other token, and the tail past the buffer, is untouched
+        np.testing.assert_array_equal(np.delete(K, band, 0), np.delete(K0, band, 0))
+        np.testing.assert_array_equal(np.delete(V, band, 0), np.delete(V0, band, 0))
+        np.testing.assert_array_equal(kvh[b, 2 * kv_tokens * H:], can[b, 2 * kv_tokens * H:])
+
+
+# ---- attention over fresh + stale K/V --------------------------------------
+
+def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fresh, seed,
+                    sample_rows=None):
+    H = heads * d
+    R = int(np.sqrt(n_kv))
+    hdr = {"hidden": H, "heads": heads, "grid": R}
+    rng = np.random.default_rng(seed)
+    scale = 0.02 * np.sqrt(1152)
+    q = rng.standard_normal((B, n_q, H)) * scale
+    Ks = rng.standard_normal((B, n_kv, H)) * scale
+    Vs = rng.standard_normal((B, n_kv, H))
+    Kf = rng.standard_normal((B, max(n_fresh, 1), H)) * scale
+    Vf = rng.standard_normal((B, max(n_fresh, 1), H))
+    qd = to_dev(np.stack([q[b].reshape(n_q, heads, d).transpose(1, 0, 2) for b in range(B)]), dtype)
+    stale = np.concatenate([dit.kv_to_buffer_layout(hdr, Ks[b], Vs[b]) for b in range(B)])
+    fresh = np.concatenate([dit.kv_to_buffer_layout(hdr, Kf[b], Vf[b]) for b in range(B)])
+    out = empty((B, n_q, H), dtype)
+    orch_lib.attention(qd, to_dev(stale, dtype), 2 * n_kv * H, to_dev(fresh, dtype),
+                       2 * max(n_fresh, 1) * H, fresh_begin, n_fresh, B, heads, n_q, n_kv, d, out,
+                       code(dtype))
+    got = to_host(out)
+    rows = np.arange(n_q) if sample_rows is None else sample_rows
+    errs = []
+    for b in range(B):
+        K, V = rounded(Ks[b], dtype), rounded(Vs[b], dtype)
+        if n_fresh:
+            K, V = dit.assemble_kv((K, V), rounded(Kf[b][:n_fresh], dtype),
+                                   rounded(Vf[b][:n_fresh], dtype), fresh_begin)
+        ref = dit.attention(rounded(q[b][rows], dtype), K, V, heads)
+        errs.append(rel_l2(got[b][rows], ref))
+    return max(errs)
+
+
+@pytest.mark.parametrize("dtype,heads,d,n_q,n_kv,fb,nf", [
+    ("f32", 4, 32, 32, 64, 0, 32),
+    ("f32", 4, 32, 20, 64, 24, 0),
+    ("bf16", 6, 64, 96, 256, 96, 96),
+    ("bf16", 6, 64, 100, 256, 0, 0),
+    ("bf16", 16, 72, 384, 1024, 640, 384),
+    ("bf16", 16, 72, 130, 1024, 8, 128),
+    ("bf16", 2, 72, 1, 64, 0, 0),
+])
+def test_attention(orch_lib, dtype, heads, d, n_q, n_kv, fb, nf):
+    err = _attention_case(orch_lib, dtype, 2, heads, d, n_q, n_kv, fb, nf, seed=n_q + n_kv + d)
+    assert err <= (1e-5 if dtype == "f32" else 1e-2), err
+
+
+def test_attention_full_xl_shape_sampled(orch_lib):
+    """DiT-XL/2 1024px, 40% band: 1664 queries x 4096 keys, 16 heads, d = 72."""
+    rows = np.r_[np.arange(0, 1664, 97), 1663]
+    err = _attention_case(orch_lib, "bf16", 2, 16, 72, 1664, 4096, 0, 1664, seed=5, sample_rows=rows)
+    assert err <= 1e-2, err
+
+
+# ---- conditioning, patch embedding, final layer -----------------------------
+
+def _ctx(orch_lib, cfg):
+    blob = generate.make_weight_blob(cfg, 0)
+    ctx = orch_lib.DiTStep(cfg, blob)
+    hdr, params = oblob.read_blob(blob)
+    return ctx, hdr, params
+
+
+@pytest.mark.parametrize("cfg", [configs.TINY, configs.DIT_S2_256,
+                                 configs.scaled(configs.DIT_XL2_512, n_blocks=3)],
+                         ids=lambda c: c.name)
+def test_conditioning(orch_lib, cfg):
+    ctx, hdr, params = _ctx(orch_lib, cfg)
+    labels = generate.make_labels(cfg, 0)
+    H, L = cfg.hidden, cfg.n_blocks
+    out = empty((cfg.cfg_batch, 6 * H * L + 2 * H))
+    for t in (0, 500, 999):
+        ctx.conditioning(t, labels, out)
+        c = dit.conditioning(hdr, params, t, labels)
+        blocks, fin = dit.adaln_vectors(hdr, params, c)
+        ref = np.concatenate([np.concatenate(blk, axis=1) for blk in blocks] + list(fin), axis=1)
+        err = rel_l2(to_host(out), ref)
+        assert err <= 1e-5, (t, err)
+
+
+@pytest.mark.parametrize("cfg,rb,re", [(configs.TINY, 0, 4), (configs.TINY, 3, 8),
+                                       (configs.DIT_S2_256, 5, 11)], ids=str)
+def test_patch_embed(orch_lib, cfg, rb, re):
+    ctx, hdr, params = _ctx(orch_lib, cfg)
+    x = generate.make_latent(cfg, 0)
+    n_tok = (re - rb) * cfg.R
+    out = empty((cfg.cfg_batch, n_tok, cfg.hidden))
+    ctx.patch_embed(to_dev(x), rb, re, out)
+    ref = dit.patch_embed(hdr, params, x.astype(np.float64), rb, re)
+    got = to_host(out)
+    for b in range(cfg.cfg_batch):
+        assert rel_l2(got[b], ref) <= 1e-6
+
+
+@pytest.mark.parametrize("cfg,rb,re", [(configs.TINY, 2, 6), (configs.DIT_S2_256, 0, 6),
+                                       (configs.scaled(configs.DIT_XL2_512, n_blocks=1), 10, 22)],
+                         ids=str)
+def test_final_layer(orch_lib, cfg, rb, re):
+    ctx, hdr, params = _ctx(orch_lib, cfg)
+    rng = np.random.default_rng(rb)
+    n_tok = (re - rb) * cfg.R
+    H, L, B = cfg.hidden, cfg.n_blocks, cfg.cfg_batch
+    h = rng.standard_normal((B, n_tok, H))
+    mod = rng.standard_normal((B, 6 * H * L + 2 * H)) * 0.1
+    out = empty((B, cfg.out_ch, (re - rb) * cfg.patch, cfg.latent))
+    ctx.final_layer(to_dev(h), rb, re, to_dev(mod), out)
+    got = to_host(out)
+    hr, mr = rounded(h, "f32"), rounded(mod, "f32")
+    for b in range(B):
+        y = dit.final_layer(hdr, params, hr[b], mr[b, 6 * H * L:6 * H * L + H], mr[b, 6 * H * L + H:])
+        ref = dit.unpatchify_rows(hdr, y, re - rb)
+        assert rel_l2(got[b], ref) <= (1e-6 if cfg.dtype == "f32" else 1e-2)
+
+
+# ---- guidance + scheduler update --------------------------------------------
+
+@pytest.mark.parametrize("n", [1, 7, 4096, 26624, (1 << 20) + 3])
+@pytest.mark.parametrize("guided,noise", [(False, False), (True, False), (True, True)])
+def test_scheduler_update(orch_lib, n, guided, noise):
+    rng = np.random.default_rng(n)
+    x, ec, eu, z = (rng.standard_normal(n).astype(np.float32) for _ in range(4))
+    t, tp = 780, 760
+    eta = 0.5 if noise else 0.0
+    a, b, c = osched.ddim_coefficients(osched.alpha_bar(), t, tp, eta)
+    out = empty((n,))
+    orch_lib.scheduler_update(to_dev(x), to_dev(ec), to_dev(eu) if guided else None, 1.5,
+                              to_dev(z) if noise else None, a, b, c, out)
+    e = dit.guided_eps(np.stack([ec, eu]).astype(np.float64), 1.5) if guided else ec.astype(np.float64)
+    ref = osched.scheduler_update(x, e, a, b, c, z if noise else None)
+    assert rel_l2(to_host(out), ref) <= 1e-6
