@@ -5,11 +5,17 @@
 // bf16 path: a flash-style kernel on v_mfma_f32_32x32x16_bf16.  Each
 // workgroup owns 128 queries of one (branch, head); each wave 32 of them.
 // Scores are formed transposed, S^T = K Q^T, so that a lane owns one query
-// column: the running max / sum of the online softmax stay in-lane, and the
-// probabilities it holds are directly the B operand of O^T = V^T P^T.  K
-// tiles ([64 keys][d]) and V^T tiles ([d][64 keys]) are staged through
+// column: the running max of the online softmax stays in-lane, and the
+// probabilities it holds are directly the B operand of O^T = V^T P^T.
+// K tiles ([64 keys][d]) and V^T tiles ([d][64 keys]) are staged through
 // double-buffered LDS; the V^T layout of the buffer makes both tile loads
-// contiguous 16-byte rows.
+// contiguous 16-byte rows.  In LDS the keys of each 16-key chunk of V^T are
+// permuted so that the 8 keys a lane's P fragment covers are contiguous (one
+// ds_read_b128), and row strides are chosen for the 64-bank LDS.  When the
+// head dimension is padded (d = 72 -> 96 rows of O^T), one padding row of
+// V^T holds ones, so the PV product also accumulates the softmax
+// denominator.  exp2 runs on v_exp_f32 with log2(e)/sqrt(d) folded into the
+// exponent; the O rescale is skipped when no lane's running max moved.
 //
 // fp32 path (and unsupported shapes): one thread per query, online softmax.
 #include "common.h"
@@ -19,22 +25,95 @@ namespace orch {
 
 namespace mfma_attn {
 constexpr int BQ = 128, BKV = 64;
-}
+
+template <int D>
+struct Geo {
+  static constexpr int DP = (D + 15) / 16 * 16;  // QK^T contraction, padded to 16
+  static constexpr int NC = DP / 16;
+  static constexpr int DV = (D + 31) / 32 * 32;  // rows of O^T, padded to 32
+  static constexpr int NT = DV / 32;
+  static constexpr bool ONES = DV > D;           // padding row D of V^T holds 1.0
+  // LDS strides in bf16: 16 consecutive rows of a 16-byte column hit 16
+  // distinct 4-bank groups (row stride = 4 * odd banks)
+  static constexpr int KS = ((DP / 2) % 8 == 4) ? DP : DP + 8;
+  static constexpr int VS = BKV + 8;
+  static constexpr int K_CHUNKS = BKV * (D / 8);
+  static constexpr int V_CHUNKS = D * (BKV / 8);
+  static constexpr int K_IT = (K_CHUNKS + 255) / 256;
+  static constexpr int V_IT = (V_CHUNKS + 255) / 256;
+};
+
+// Register staging of one K tile ([64 keys][D]) and one V^T tile ([D][64
+// keys]) for 256 threads.  K chunk c: key row c / (D/8), 8-dim chunk c % (D/8).
+// V^T chunk c: dim row c / 8, 8-key chunk kc = c % 8; in LDS the 4+4 keys of
+// that chunk go to positions (kc/2)*16 + (kc%2)*4 and +8, so that within a
+// 16-key group a lane with half h finds keys {4h..4h+3, 8+4h..8+4h+3}
+// contiguous.  Idle slots re-read a valid chunk and skip the store.
+template <int D>
+struct Stage {
+  using G = Geo<D>;
+  int k_row[G::K_IT], k_col[G::K_IT], v_row[G::V_IT], v_kc[G::V_IT], v_dst[G::V_IT];
+  bool k_on[G::K_IT], v_on[G::V_IT];
+  uint4 rk[G::K_IT], rv[G::V_IT];
+
+  __device__ __forceinline__ void init(int tid) {
+#pragma unroll
+    for (int i = 0; i < G::K_IT; ++i) {
+      const int c = tid + 256 * i;
+      k_on[i] = c < G::K_CHUNKS;
+      k_row[i] = k_on[i] ? c / (D / 8) : 0;
+      k_col[i] = k_on[i] ? (c % (D / 8)) * 8 : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < G::V_IT; ++i) {
+      const int c = tid + 256 * i;
+      v_on[i] = c < G::V_CHUNKS;
+      v_row[i] = v_on[i] ? c >> 3 : 0;
+      v_kc[i] = v_on[i] ? c & 7 : 0;
+      v_dst[i] = v_row[i] * G::VS + (v_kc[i] >> 1) * 16 + (v_kc[i] & 1) * 4;
+    }
+  }
+  __device__ __forceinline__ void load(int n0, const AttnParams& p, const bf16* kf,
+                                       const bf16* ks, const bf16* vf, const bf16* vs) {
+#pragma unroll
+    for (int i = 0; i < G::K_IT; ++i) {
+      const int n = n0 + k_row[i];
+      const int f = n - p.fresh_begin;
+      const bf16* src = ((unsigned)f < (unsigned)p.n_fresh) ? kf + (size_t)f * D : ks + (size_t)n * D;
+      rk[i] = *reinterpret_cast<const uint4*>(src + k_col[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < G::V_IT; ++i) {
+      const int n = n0 + v_kc[i] * 8;
+      const int f = n - p.fresh_begin;
+      const bf16* src = ((unsigned)f < (unsigned)p.n_fresh)
+                            ? vf + (size_t)v_row[i] * p.n_fresh + f
+                            : vs + (size_t)v_row[i] * p.n_kv + n;
+      rv[i] = *reinterpret_cast<const uint4*>(src);
+    }
+  }
+  __device__ __forceinline__ void store(bf16* sk, bf16* sv) const {
+#pragma unroll
+    for (int i = 0; i < G::K_IT; ++i)
+      if (k_on[i]) *reinterpret_cast<uint4*>(sk + k_row[i] * G::KS + k_col[i]) = rk[i];
+#pragma unroll
+    for (int i = 0; i < G::V_IT; ++i)
+      if (v_on[i]) {
+        *reinterpret_cast<uint2*>(sv + v_dst[i]) = make_uint2(rv[i].x, rv[i].y);
+        *reinterpret_cast<uint2*>(sv + v_dst[i] + 8) = make_uint2(rv[i].z, rv[i].w);
+      }
+  }
+};
+
+}  // namespace mfma_attn
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
   using namespace mfma_attn;
-  constexpr int DP = (D + 15) / 16 * 16;         // QK^T contraction, padded to 16
-  constexpr int NC = DP / 16;
-  constexpr int DV = (D + 31) / 32 * 32;         // rows of O^T, padded to 32
-  constexpr int NT = DV / 32;
-  constexpr int KS = (DP % 64 == 0) ? DP + 8 : DP;  // LDS row stride of K tiles
-  constexpr int VS = BKV + 8;                        // LDS row stride of V^T tiles
-  constexpr int KCH = D / 8;                         // 16-byte chunks per K row
-  constexpr int K_CHUNKS = BKV * KCH;
-  constexpr int V_CHUNKS = D * (BKV / 8);
-  constexpr int K_IT = (K_CHUNKS + 255) / 256;
-  constexpr int V_IT = (V_CHUNKS + 255) / 256;
+  using G = Geo<D>;
+  constexpr int NC = G::NC, NT = G::NT, DV = G::DV, KS = G::KS, VS = G::VS;
+  constexpr int K_IT = G::K_IT, V_IT = G::V_IT;
+  static_assert(((KS / 2) % 4 == 0) && (((KS / 2) / 4) % 2 == 1), "K stride");
 
   __shared__ __attribute__((aligned(16))) bf16 sK[2][BKV * KS];
   __shared__ __attribute__((aligned(16))) bf16 sV[2][DV * VS];
@@ -54,25 +133,27 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
                    (size_t)head * p.n_kv * D;
   const bf16* vs = reinterpret_cast<const bf16*>(p.kv_stale) + b * p.stale_bs +
                    (size_t)p.n_kv * H + (size_t)head * D * p.n_kv;
-  const bf16* kf = nullptr;
-  const bf16* vf = nullptr;
+  const bf16* kf = ks;
+  const bf16* vf = vs;
   if (p.n_fresh > 0) {
     kf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)head * p.n_fresh * D;
     vf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)p.n_fresh * H +
          (size_t)head * D * p.n_fresh;
   }
 
-  // zero the padding columns of K and rows of V^T once (never overwritten)
+  // padding: K columns [D, KS) are zero; V^T rows [D, DV) are zero except
+  // row D, which is one when present (never overwritten by tile loads)
   for (int i = tid; i < 2 * BKV * (KS - D); i += 256) {
-    int buf = i / (BKV * (KS - D));
-    int rem = i - buf * BKV * (KS - D);
-    int r = rem / (KS - D), c = D + rem % (KS - D);
-    sK[buf][r * KS + c] = (bf16)0.0f;
+    const int buf = i / (BKV * (KS - D));
+    const int rem = i - buf * BKV * (KS - D);
+    sK[buf][(rem / (KS - D)) * KS + D + rem % (KS - D)] = (bf16)0.0f;
   }
-  for (int i = tid; i < 2 * (DV - D) * VS; i += 256) {
-    int buf = i / ((DV - D) * VS);
-    int rem = i - buf * (DV - D) * VS;
-    sV[buf][D * VS + rem] = (bf16)0.0f;
+  if constexpr (DV > D) {
+    for (int i = tid; i < 2 * (DV - D) * VS; i += 256) {
+      const int buf = i / ((DV - D) * VS);
+      const int rem = i - buf * (DV - D) * VS;
+      sV[buf][D * VS + rem] = (bf16)(rem < VS ? 1.0f : 0.0f);
+    }
   }
 
   // this lane's query (B operand of S^T = K Q^T): Q[q][c*16 + 8h .. +8]
@@ -89,51 +170,8 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
     }
   }
 
-  uint4 rk[K_IT], rv[V_IT];
-  auto load_kv = [&](int n0) {
-#pragma unroll
-    for (int i = 0; i < K_IT; ++i) {
-      int c = tid + 256 * i;
-      if (c < K_CHUNKS) {
-        int r = c / KCH, cc = c - r * KCH;
-        int n = n0 + r;
-        int f = n - p.fresh_begin;
-        const bf16* src = ((unsigned)f < (unsigned)p.n_fresh) ? kf + (size_t)f * D : ks + (size_t)n * D;
-        rk[i] = *reinterpret_cast<const uint4*>(src + cc * 8);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < V_IT; ++i) {
-      int c = tid + 256 * i;
-      if (c < V_CHUNKS) {
-        int d = c >> 3, kc = c & 7;
-        int n = n0 + kc * 8;
-        int f = n - p.fresh_begin;
-        const bf16* src = ((unsigned)f < (unsigned)p.n_fresh) ? vf + (size_t)d * p.n_fresh + f
-                                                              : vs + (size_t)d * p.n_kv + n;
-        rv[i] = *reinterpret_cast<const uint4*>(src);
-      }
-    }
-  };
-  auto store_kv = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < K_IT; ++i) {
-      int c = tid + 256 * i;
-      if (c < K_CHUNKS) {
-        int r = c / KCH, cc = c - r * KCH;
-        *reinterpret_cast<uint4*>(&sK[buf][r * KS + cc * 8]) = rk[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < V_IT; ++i) {
-      int c = tid + 256 * i;
-      if (c < V_CHUNKS) {
-        int d = c >> 3, kc = c & 7;
-        *reinterpret_cast<uint4*>(&sV[buf][d * VS + kc * 8]) = rv[i];
-      }
-    }
-  };
-
+  Stage<D> stg;
+  stg.init(tid);
   const float scale = 1.4426950408889634f / sqrtf((float)D);  // log2(e) / sqrt(d)
   float m_run = -1e30f, l_run = 0.0f;
   f32x16 o[NT];
@@ -142,14 +180,17 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
 
+  const int k_rd = lc * KS + h * 8;   // + sub*32*KS + c*16
+  const int v_rd = lc * VS + h * 8;   // + t*32*VS + c*16
+
   const int NIT = p.n_kv / BKV;
-  load_kv(0);
-  store_kv(0);
+  stg.load(0, p, kf, ks, vf, vs);
+  stg.store(sK[0], sV[0]);
   __syncthreads();
 
   for (int it = 0; it < NIT; ++it) {
     const int buf = it & 1;
-    if (it + 1 < NIT) load_kv((it + 1) * BKV);
+    stg.load((it + 1 < NIT ? it + 1 : it) * BKV, p, kf, ks, vf, vs);
 
     // S^T for keys [32 sub, 32 sub + 32) x this wave's 32 queries
     f32x16 s[2];
@@ -159,19 +200,18 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
       for (int r = 0; r < 16; ++r) s[sub][r] = 0.0f;
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
-        bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[buf][(sub * 32 + lc) * KS + c * 16 + h * 8]);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[buf][k_rd + sub * 32 * KS + c * 16]);
         s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[c], s[sub], 0, 0, 0);
       }
     }
     // online softmax over this lane's query column
-    float mx = s[0][0];
+    float mx = fmaxf(s[0][0], s[1][0]);
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[sub][r]);
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
     const float m_new = fmaxf(m_run, mx * scale);
-    const float alpha = exp2f(m_run - m_new);
+    const bool moved = m_new > m_run;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     m_run = m_new;
     float psum = 0.0f;
     bf16x8 pf[4];
@@ -182,39 +222,42 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int r = 4 * (g0 + (e >> 2)) + (e & 3);
-        const float pv = exp2f(fmaf(s[sub][r], scale, -m_new));
-        psum += pv;
+        const float pv = __builtin_amdgcn_exp2f(fmaf(s[sub][r], scale, -m_new));
+        if constexpr (!G::ONES) psum += pv;
         pf[c][e] = (bf16)pv;
       }
     }
-    l_run = l_run * alpha + psum;
+    if constexpr (!G::ONES) l_run = l_run * alpha + psum;
+    if (__any(moved)) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+    }
 
     // O^T += V^T P^T
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const bf16* vrow = &sV[buf][(t * 32 + lc) * VS + c * 16 + 4 * h];
-        bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-        bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 8);
-        bf16x8 a;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a[e] = lo[e];
-          a[e + 4] = hi[e];
-        }
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sV[buf][v_rd + t * 32 * VS + c * 16]);
         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[c], o[t], 0, 0, 0);
       }
     }
-    if (it + 1 < NIT) store_kv(buf ^ 1);
+    if (it + 1 < NIT) stg.store(sK[buf ^ 1], sV[buf ^ 1]);
     __syncthreads();
   }
 
-  const float l = l_run + __shfl_xor(l_run, 32, kWave);
+  // softmax denominator: the ones row D of O^T (register 4*((D%32)/8) + D%4
+  // of tile D/32 on the h == 0 lanes), or the running sum
+  float l;
+  if constexpr (G::ONES) {
+    constexpr int TR = D / 32, RR = 4 * ((D % 32) / 8) + (D % 4);
+    static_assert(((D % 32) / 4) % 2 == 0, "ones row on the h == 0 half");
+    l = __shfl(o[TR][RR], lc, kWave);
+  } else {
+    l = l_run + __shfl_xor(l_run, 32, kWave);
+  }
   const float inv = 1.0f / l;
   const int q = q0 + wave * 32 + lc;
   if (q < p.n_q) {
