@@ -166,11 +166,19 @@ int orch_op_qkv_projection(const void* A, int B, int n_tok, int K, const void* W
  * fresh_begin + n_fresh (fresh token n - fresh_begin; K [heads][n_fresh][d],
  * V at offset n_fresh*H as [heads][d][n_fresh], branch stride
  * fresh_branch_stride) and from `kv_stale` otherwise (buffer layout, branch
- * stride stale_branch_stride).  n_fresh may be 0.  out T [B][n_q][H]. */
+ * stride stale_branch_stride).  n_fresh may be 0.  out T [B][n_q][H].
+ * workspace: device memory of at least orch_attention_workspace_bytes() bytes
+ * lets short bands split the keys over more workgroups; NULL (or fewer
+ * bytes) runs unsplit.  The result does not depend on the split beyond
+ * rounding. */
 int orch_op_attention(const void* q, const void* kv_stale, size_t stale_branch_stride,
                       const void* kv_fresh, size_t fresh_branch_stride, int fresh_begin,
                       int n_fresh, int B, int heads, int n_q, int n_kv, int head_dim, void* out,
-                      int dtype, void* hip_stream);
+                      void* workspace, size_t workspace_bytes, int dtype, void* hip_stream);
+
+/* Workspace bytes orch_op_attention can use for this shape (0: never splits). */
+size_t orch_attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int head_dim,
+                                      int dtype);
 
 /* Conditioning of the loaded model: out fp32 [cfg_batch][6*H*n_blocks + 2*H],
  * the adaLN vectors of every block followed by the final layer's

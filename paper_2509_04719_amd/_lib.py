@@ -23,6 +23,7 @@ SYMBOLS = (
     "orch_patch_denoise_step", "orch_scheduler_update", "orch_schedule_coefficients",
     "orch_last_error", "orch_op_layernorm_modulate", "orch_op_linear", "orch_op_qkv_projection",
     "orch_op_attention", "orch_op_conditioning", "orch_op_patch_embed", "orch_op_final_layer",
+    "orch_attention_workspace_bytes",
 )
 
 
@@ -66,7 +67,8 @@ def _load():
         "orch_op_layernorm_modulate": (i, [vp, i, i, i, vp, vp, i, vp, i, vp]),
         "orch_op_linear": (i, [vp, i, i, vp, i, vp, i, vp, i, i, vp, i, vp]),
         "orch_op_qkv_projection": (i, [vp, i, i, i, vp, vp, i, i, vp, vp, sz, i, i, i, vp]),
-        "orch_op_attention": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, i, vp]),
+        "orch_op_attention": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, vp, sz, i, vp]),
+        "orch_attention_workspace_bytes": (sz, [i, i, i, i, i, i]),
         "orch_op_conditioning": (i, [vp, i, C.POINTER(i), vp, vp]),
         "orch_op_patch_embed": (i, [vp, vp, i, i, vp, vp]),
         "orch_op_final_layer": (i, [vp, vp, i, i, vp, vp, vp]),
@@ -183,8 +185,13 @@ def qkv_projection(A, B, n_tok, K, W, bias, hidden, heads, q_out, kv_out, kv_bra
                                      tok_offset, dtype, _stream(stream)))
 
 
+def attention_workspace_bytes(B, heads, n_q, n_kv, head_dim, dtype) -> int:
+    return lib.orch_attention_workspace_bytes(B, heads, n_q, n_kv, head_dim, dtype)
+
+
 def attention(q, kv_stale, stale_bs, kv_fresh, fresh_bs, fresh_begin, n_fresh, B, heads, n_q,
-              n_kv, head_dim, out, dtype, stream=None):
+              n_kv, head_dim, out, dtype, workspace=None, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     check(lib.orch_op_attention(_ptr(q), _ptr(kv_stale), stale_bs, _ptr(kv_fresh), fresh_bs,
                                 fresh_begin, n_fresh, B, heads, n_q, n_kv, head_dim, _ptr(out),
-                                dtype, _stream(stream)))
+                                _ptr(workspace), ws_bytes, dtype, _stream(stream)))

@@ -20,6 +20,10 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liborch.so")
 SOURCES = ["k_gemm.hip", "k_attention.hip", "k_misc.hip", "orch_abi.hip"]
+# per-source extra flags: attention keeps MFMA accumulators in VGPRs (its
+# softmax works on the scores with VALU ops, which would otherwise copy them
+# out of AGPRs every tile)
+EXTRA = {"k_attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 ARCH = "gfx950"
 
 
@@ -39,7 +43,7 @@ def common_flags():
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc()] + common_flags() + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc()] + common_flags() + EXTRA.get(src, []) + ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -15,7 +15,9 @@
 // head dimension is padded (d = 72 -> 96 rows of O^T), one padding row of
 // V^T holds ones, so the PV product also accumulates the softmax
 // denominator.  exp2 runs on v_exp_f32 with log2(e)/sqrt(d) folded into the
-// exponent; the O rescale is skipped when no lane's running max moved.
+// exponent; the running max is raised lazily (only past a 2^8 margin), so
+// O is rarely rescaled.  Built with MFMA accumulators in VGPRs, so the
+// softmax reads the scores without AGPR copies.
 //
 // fp32 path (and unsupported shapes): one thread per query, online softmax.
 #include "common.h"
@@ -41,6 +43,7 @@ struct Geo {
   static constexpr int V_CHUNKS = D * (BKV / 8);
   static constexpr int K_IT = (K_CHUNKS + 255) / 256;
   static constexpr int V_IT = (V_CHUNKS + 255) / 256;
+  static constexpr int K_BUF = BKV * KS, V_BUF = DV * VS;
 };
 
 // Register staging of one K tile ([64 keys][D]) and one V^T tile ([D][64
@@ -48,12 +51,13 @@ struct Geo {
 // V^T chunk c: dim row c / 8, 8-key chunk kc = c % 8; in LDS the 4+4 keys of
 // that chunk go to positions (kc/2)*16 + (kc%2)*4 and +8, so that within a
 // 16-key group a lane with half h finds keys {4h..4h+3, 8+4h..8+4h+3}
-// contiguous.  Idle slots re-read a valid chunk and skip the store.
+// contiguous.  Idle slots (the tile does not split evenly over 256 threads)
+// re-read a valid chunk and skip the store.
 template <int D>
 struct Stage {
   using G = Geo<D>;
-  int k_row[G::K_IT], k_col[G::K_IT], v_row[G::V_IT], v_kc[G::V_IT], v_dst[G::V_IT];
-  bool k_on[G::K_IT], v_on[G::V_IT];
+  int k_row[G::K_IT], k_col[G::K_IT], k_dst[G::K_IT], v_row[G::V_IT], v_kc[G::V_IT],
+      v_dst[G::V_IT], k_on[G::K_IT], v_on[G::V_IT];
   uint4 rk[G::K_IT], rv[G::V_IT];
 
   __device__ __forceinline__ void init(int tid) {
@@ -63,6 +67,7 @@ struct Stage {
       k_on[i] = c < G::K_CHUNKS;
       k_row[i] = k_on[i] ? c / (D / 8) : 0;
       k_col[i] = k_on[i] ? (c % (D / 8)) * 8 : 0;
+      k_dst[i] = k_row[i] * G::KS + k_col[i];
     }
 #pragma unroll
     for (int i = 0; i < G::V_IT; ++i) {
@@ -73,8 +78,8 @@ struct Stage {
       v_dst[i] = v_row[i] * G::VS + (v_kc[i] >> 1) * 16 + (v_kc[i] & 1) * 4;
     }
   }
-  __device__ __forceinline__ void load(int n0, const AttnParams& p, const bf16* kf,
-                                       const bf16* ks, const bf16* vf, const bf16* vs) {
+  __device__ __forceinline__ void load_k(int n0, const AttnParams& p, const bf16* kf,
+                                         const bf16* ks) {
 #pragma unroll
     for (int i = 0; i < G::K_IT; ++i) {
       const int n = n0 + k_row[i];
@@ -82,6 +87,9 @@ struct Stage {
       const bf16* src = ((unsigned)f < (unsigned)p.n_fresh) ? kf + (size_t)f * D : ks + (size_t)n * D;
       rk[i] = *reinterpret_cast<const uint4*>(src + k_col[i]);
     }
+  }
+  __device__ __forceinline__ void load_v(int n0, const AttnParams& p, const bf16* vf,
+                                         const bf16* vs) {
 #pragma unroll
     for (int i = 0; i < G::V_IT; ++i) {
       const int n = n0 + v_kc[i] * 8;
@@ -92,10 +100,12 @@ struct Stage {
       rv[i] = *reinterpret_cast<const uint4*>(src);
     }
   }
-  __device__ __forceinline__ void store(bf16* sk, bf16* sv) const {
+  __device__ __forceinline__ void store_k(bf16* sk) const {
 #pragma unroll
     for (int i = 0; i < G::K_IT; ++i)
-      if (k_on[i]) *reinterpret_cast<uint4*>(sk + k_row[i] * G::KS + k_col[i]) = rk[i];
+      if (k_on[i]) *reinterpret_cast<uint4*>(sk + k_dst[i]) = rk[i];
+  }
+  __device__ __forceinline__ void store_v(bf16* sv) const {
 #pragma unroll
     for (int i = 0; i < G::V_IT; ++i)
       if (v_on[i]) {
@@ -104,6 +114,28 @@ struct Stage {
       }
   }
 };
+
+// S^T of one 64-key tile: keys [32 sub, +32) x a wave's 32 queries.  `sk`
+// points at this lane's row / half of the K tile in LDS.
+struct Scores {
+  f32x16 v[2];
+};
+
+template <int D>
+__device__ __forceinline__ Scores qk_scores(const bf16* sk, const bf16x8 (&qf)[Geo<D>::NC]) {
+  Scores sc;
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc.v[sub][r] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < Geo<D>::NC; ++c) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(sk + sub * 32 * Geo<D>::KS + c * 16);
+      sc.v[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[c], sc.v[sub], 0, 0, 0);
+    }
+  }
+  return sc;
+}
 
 }  // namespace mfma_attn
 
@@ -115,8 +147,8 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
   constexpr int K_IT = G::K_IT, V_IT = G::V_IT;
   static_assert(((KS / 2) % 4 == 0) && (((KS / 2) / 4) % 2 == 1), "K stride");
 
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][BKV * KS];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][DV * VS];
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][G::K_BUF];
+  __shared__ __attribute__((aligned(16))) bf16 sV[2][G::V_BUF];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -125,8 +157,12 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
   const int lc = lane & 31;
   const int b = blockIdx.z;
   const int head = blockIdx.y;
-  const int q0 = blockIdx.x * BQ;
+  const int n_qt = (p.n_q + BQ - 1) / BQ;
+  const int split = blockIdx.x / n_qt;            // key split of this workgroup
+  const int q0 = (blockIdx.x - split * n_qt) * BQ;
   const int H = p.heads * D;
+  const int kv_len = p.n_kv / p.splits;           // multiple of BKV (launcher)
+  const int kv0 = split * kv_len;
 
   const bf16* qbase = reinterpret_cast<const bf16*>(p.q) + ((size_t)b * p.heads + head) * p.n_q * D;
   const bf16* ks = reinterpret_cast<const bf16*>(p.kv_stale) + b * p.stale_bs +
@@ -183,36 +219,42 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
   const int k_rd = lc * KS + h * 8;   // + sub*32*KS + c*16
   const int v_rd = lc * VS + h * 8;   // + t*32*VS + c*16
 
-  const int NIT = p.n_kv / BKV;
-  stg.load(0, p, kf, ks, vf, vs);
-  stg.store(sK[0], sV[0]);
+  // Key tiles: K and V^T of tile it in sK / sV[it & 1]; the next tile is
+  // loaded into registers during this one and stored before the barrier.
+  // The loads are unconditional (past the end they re-read the last tile,
+  // which is then not stored) so the staging stays in registers.
+  const int NIT = kv_len / BKV;
+  stg.load_k(kv0, p, kf, ks);
+  stg.load_v(kv0, p, vf, vs);
+  stg.store_k(sK[0]);
+  stg.store_v(sV[0]);
   __syncthreads();
 
   for (int it = 0; it < NIT; ++it) {
     const int buf = it & 1;
-    stg.load((it + 1 < NIT ? it + 1 : it) * BKV, p, kf, ks, vf, vs);
+    stg.load_k(kv0 + min(it + 1, NIT - 1) * BKV, p, kf, ks);
+    stg.load_v(kv0 + min(it + 1, NIT - 1) * BKV, p, vf, vs);
+    const Scores sc = qk_scores<D>(sK[buf] + k_rd, qf);
 
-    // S^T for keys [32 sub, 32 sub + 32) x this wave's 32 queries
-    f32x16 s[2];
+    // online softmax over this lane's query column.  The running max is only
+    // raised when some lane's tile max exceeds it by more than 8 (log2
+    // units): until then exp2(s - m_run) <= 2^8, exact in fp32 and in range
+    // for bf16, and O and the denominator keep a common scale, so O is
+    // rarely rescaled.
+    float mx = fmaxf(sc.v[0][0], sc.v[1][0]);
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sc.v[0][r], sc.v[1][r]));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale;
+    float alpha = 1.0f;
+    if (__any(mx > m_run + 8.0f)) {
+      const float m_new = fmaxf(m_run, mx);
+      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[sub][r] = 0.0f;
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[buf][k_rd + sub * 32 * KS + c * 16]);
-        s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[c], s[sub], 0, 0, 0);
-      }
+        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
     }
-    // online softmax over this lane's query column
-    float mx = fmaxf(s[0][0], s[1][0]);
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float m_new = fmaxf(m_run, mx * scale);
-    const bool moved = m_new > m_run;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
     float psum = 0.0f;
     bf16x8 pf[4];
 #pragma unroll
@@ -222,29 +264,27 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int r = 4 * (g0 + (e >> 2)) + (e & 3);
-        const float pv = __builtin_amdgcn_exp2f(fmaf(s[sub][r], scale, -m_new));
+        const float pv = __builtin_amdgcn_exp2f(fmaf(sc.v[sub][r], scale, -m_run));
         if constexpr (!G::ONES) psum += pv;
         pf[c][e] = (bf16)pv;
       }
     }
     if constexpr (!G::ONES) l_run = l_run * alpha + psum;
-    if (__any(moved)) {
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
-    }
 
     // O^T += V^T P^T
+    const bf16* sv = sV[buf];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sV[buf][v_rd + t * 32 * VS + c * 16]);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(sv + v_rd + t * 32 * VS + c * 16);
         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[c], o[t], 0, 0, 0);
       }
     }
-    if (it + 1 < NIT) stg.store(sK[buf ^ 1], sV[buf ^ 1]);
+    if (it + 1 < NIT) {
+      stg.store_k(sK[buf ^ 1]);
+      stg.store_v(sV[buf ^ 1]);
+    }
     __syncthreads();
   }
 
@@ -258,8 +298,26 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
   } else {
     l = l_run + __shfl_xor(l_run, 32, kWave);
   }
-  const float inv = 1.0f / l;
   const int q = q0 + wave * 32 + lc;
+  if (p.splits > 1) {
+    // partial result of this key split: unnormalised O, running max and sum
+    if (q < p.n_q) {
+      float* orow = p.part_o + (((size_t)split * p.B + b) * p.n_q + q) * H + head * D;
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int d = t * 32 + 8 * g + 4 * h;
+          if (d < D)
+            *reinterpret_cast<float4*>(orow + d) =
+                make_float4(o[t][4 * g], o[t][4 * g + 1], o[t][4 * g + 2], o[t][4 * g + 3]);
+        }
+      if (h == 0)
+        p.part_ml[(((size_t)split * p.B + b) * p.heads + head) * p.n_q + q] = make_float2(m_run, l);
+    }
+    return;
+  }
+  const float inv = 1.0f / l;
   if (q < p.n_q) {
     bf16* orow = reinterpret_cast<bf16*>(p.out) + ((size_t)b * p.n_q + q) * H + head * D;
 #pragma unroll
@@ -275,6 +333,28 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
         }
       }
   }
+}
+
+// Combine of the key splits: O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s
+// (m = max_s m_s, all in the log2 domain of the kernel above).
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
+  const int H = p.heads * p.d;
+  const size_t row = blockIdx.y;                 // b * n_q + q
+  const int col = blockIdx.x * 256 + threadIdx.x;
+  if (col >= H) return;
+  const int b = (int)(row / p.n_q), q = (int)(row - (size_t)b * p.n_q);
+  const int head = col / p.d;
+  float m = -1e30f;
+  for (int s = 0; s < p.splits; ++s)
+    m = fmaxf(m, p.part_ml[(((size_t)s * p.B + b) * p.heads + head) * p.n_q + q].x);
+  float num = 0.0f, den = 0.0f;
+  for (int s = 0; s < p.splits; ++s) {
+    const float2 ml = p.part_ml[(((size_t)s * p.B + b) * p.heads + head) * p.n_q + q];
+    const float w = __builtin_amdgcn_exp2f(ml.x - m);
+    num += w * p.part_o[((size_t)s * p.B * p.n_q + row) * H + col];
+    den += w * ml.y;
+  }
+  reinterpret_cast<bf16*>(p.out)[row * H + col] = (bf16)(num / den);
 }
 
 // ---------------------------------------------------------------------------
@@ -349,15 +429,51 @@ static hipError_t launch_simt(const AttnParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnParams& p, int dtype, hipStream_t s) {
-  if (p.n_q <= 0) return hipSuccess;
+// Key splits: the largest power of two (<= 8) that keeps the workgroup count
+// within two per CU (512) and at least 4 key tiles per split.
+static int pick_splits(int B, int heads, int n_q, int n_kv) {
+  const int wg = ceil_div(n_q, mfma_attn::BQ) * heads * B;
+  const int tiles = n_kv / mfma_attn::BKV;
+  int s = 1;
+  while (s < 8 && wg * s * 2 <= 512 && tiles % (2 * s) == 0 && tiles / (2 * s) >= 4) s *= 2;
+  return s;
+}
+
+static size_t part_o_bytes(int splits, int B, int n_q, int H) {
+  return ((size_t)splits * B * n_q * H * 4 + 255) / 256 * 256;
+}
+
+size_t attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int d, int dtype) {
+  if (n_q <= 0 || !attention_uses_mfma(d, n_kv, dtype)) return 0;
+  const int s = pick_splits(B, heads, n_q, n_kv);
+  if (s == 1) return 0;
+  return part_o_bytes(s, B, n_q, heads * d) + (size_t)s * B * heads * n_q * sizeof(float2);
+}
+
+hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
+  if (p0.n_q <= 0) return hipSuccess;
+  AttnParams p = p0;
+  p.splits = 1;
   const bool aligned = (p.fresh_begin % 8 == 0) && (p.n_fresh % 8 == 0);
   if (attention_uses_mfma(p.d, p.n_kv, dtype) && aligned) {
-    dim3 grid(ceil_div(p.n_q, mfma_attn::BQ), p.heads, p.B);
+    const int want = pick_splits(p.B, p.heads, p.n_q, p.n_kv);
+    if (want > 1 && p.ws &&
+        p.ws_bytes >= attention_workspace_bytes(p.B, p.heads, p.n_q, p.n_kv, p.d, dtype)) {
+      p.splits = want;
+      p.part_o = reinterpret_cast<float*>(p.ws);
+      p.part_ml = reinterpret_cast<float2*>(reinterpret_cast<char*>(p.ws) +
+                                            part_o_bytes(want, p.B, p.n_q, p.heads * p.d));
+    }
+    dim3 grid(ceil_div(p.n_q, mfma_attn::BQ) * p.splits, p.heads, p.B);
     if (p.d == 64)
       hipLaunchKernelGGL(attn_bf16_mfma_kernel<64>, grid, dim3(256), 0, s, p);
     else
       hipLaunchKernelGGL(attn_bf16_mfma_kernel<72>, grid, dim3(256), 0, s, p);
+    if (p.splits > 1) {
+      const size_t H = (size_t)p.heads * p.d;
+      dim3 g2(ceil_div((int)H, 256), p.B * p.n_q);
+      hipLaunchKernelGGL(attn_combine_kernel, g2, dim3(256), 0, s, p);
+    }
     return hipGetLastError();
   }
   if (dtype == kBF16) return launch_simt<bf16>(p, s);

@@ -46,8 +46,18 @@ struct AttnParams {
   int fresh_begin, n_fresh;
   int B, heads, n_q, n_kv, d;
   void* out;                  // T [B][n_q][heads*d]
+  // split-KV workspace (optional): fp32 partials, see attention_workspace_bytes
+  void* ws;
+  size_t ws_bytes;
+  // set by the launcher: number of key splits and, per split, the partial
+  // outputs O_s fp32 [splits][B*n_q][H] and (max, sum) float2 [splits][B][heads][n_q]
+  int splits;
+  float* part_o;
+  float2* part_ml;
 };
 
+// Workspace bytes of the split-KV path for this shape (0: no split is used).
+size_t attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int d, int dtype);
 hipError_t launch_attention(const AttnParams& p, int dtype, hipStream_t stream);
 bool attention_uses_mfma(int d, int n_kv, int dtype);
 

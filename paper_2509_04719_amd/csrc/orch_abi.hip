@@ -2,6 +2,7 @@
 // argument validation and the per-step launch sequence (Algorithm 1: one-step
 // inference on the device's band with the stale buffer, then the buffer
 // update; the scheduler update of §I with Lemma 1's coefficient).
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -85,6 +86,8 @@ struct orch_ctx {
   float* t1 = nullptr;
   float* sc = nullptr;
   float* eps = nullptr;
+  void* attn_ws = nullptr;
+  size_t attn_ws_bytes = 0;
 };
 
 namespace {
@@ -208,14 +211,20 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
   const size_t es = esize(cfg->dtype);
   const size_t tokB = (size_t)x->B * x->n_kv;
   struct Part { size_t bytes; void** dst; };
-  void *p_h, *p_u, *p_q, *p_kvf, *p_att, *p_mlp, *p_mod, *p_t1, *p_sc, *p_eps;
+  void *p_h, *p_u, *p_q, *p_kvf, *p_att, *p_mlp, *p_mod, *p_t1, *p_sc, *p_eps, *p_aws;
+  // split-KV partials: the largest need over every band height
+  size_t aws = 0;
+  for (int r = 1; r <= x->R; ++r)
+    aws = std::max(aws, attention_workspace_bytes(x->B, x->heads, r * x->R, x->n_kv, x->d, cfg->dtype));
+  x->attn_ws_bytes = aws;
   const Part parts[] = {
       {tokB * x->H * 4, &p_h},        {tokB * x->H * es, &p_u},
       {tokB * x->H * es, &p_q},       {2 * tokB * x->H * es, &p_kvf},
       {tokB * x->H * es, &p_att},     {tokB * x->F * es, &p_mlp},
       {(size_t)x->B * x->n_mod * 4, &p_mod}, {(size_t)x->H * 4, &p_t1},
       {(size_t)x->B * x->H * 4, &p_sc},
-      {(size_t)x->B * cfg->out_ch * cfg->latent * cfg->latent * 4, &p_eps}};
+      {(size_t)x->B * cfg->out_ch * cfg->latent * cfg->latent * 4, &p_eps},
+      {aws, &p_aws}};
   size_t total = 0;
   for (const Part& p : parts) total += (p.bytes + 255) / 256 * 256;
   hipError_t e = hipMalloc(&x->ws, total);
@@ -230,6 +239,7 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
   }
   x->h = (float*)p_h; x->u = p_u; x->q = p_q; x->kvf = p_kvf; x->att = p_att; x->mlp = p_mlp;
   x->mod = (float*)p_mod; x->t1 = (float*)p_t1; x->sc = (float*)p_sc; x->eps = (float*)p_eps;
+  x->attn_ws = aws ? p_aws : nullptr;
   *out = x;
   return ORCH_OK;
 }
@@ -515,6 +525,7 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
     ap.kv_fresh = refresh ? nullptr : x->kvf; ap.fresh_bs = fresh_bs;
     ap.fresh_begin = refresh ? 0 : rb * x->R; ap.n_fresh = refresh ? 0 : n_tok;
     ap.B = B; ap.heads = x->heads; ap.n_q = n_tok; ap.n_kv = x->n_kv; ap.d = x->d; ap.out = x->att;
+    ap.ws = x->attn_ws; ap.ws_bytes = x->attn_ws_bytes;
     HIP_TRY(launch_attention(ap, dt, s), "attention launch");
 
     EpiParams eo{};
@@ -617,9 +628,16 @@ int orch_op_qkv_projection(const void* A, int B, int n_tok, int K, const void* W
   return ORCH_OK;
 }
 
+size_t orch_attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int head_dim,
+                                      int dtype) {
+  if (B < 1 || heads < 1 || n_q < 0 || n_kv < 1 || head_dim < 1) return 0;
+  return attention_workspace_bytes(B, heads, n_q, n_kv, head_dim, dtype);
+}
+
 int orch_op_attention(const void* q, const void* kv_stale, size_t stale_bs, const void* kv_fresh,
                       size_t fresh_bs, int fresh_begin, int n_fresh, int B, int heads, int n_q,
-                      int n_kv, int head_dim, void* out, int dtype, void* hip_stream) {
+                      int n_kv, int head_dim, void* out, void* workspace, size_t workspace_bytes,
+                      int dtype, void* hip_stream) {
   if (!q || !kv_stale || !out || (n_fresh > 0 && !kv_fresh)) return fail(ORCH_EINVAL, "NULL pointer");
   if (B < 1 || heads < 1 || n_q < 0 || n_kv < 1 || n_fresh < 0 || fresh_begin < 0 ||
       fresh_begin + n_fresh > n_kv)
@@ -635,6 +653,7 @@ int orch_op_attention(const void* q, const void* kv_stale, size_t stale_bs, cons
   ap.q = q; ap.kv_stale = kv_stale; ap.stale_bs = stale_bs; ap.kv_fresh = kv_fresh;
   ap.fresh_bs = fresh_bs; ap.fresh_begin = fresh_begin; ap.n_fresh = n_fresh; ap.B = B;
   ap.heads = heads; ap.n_q = n_q; ap.n_kv = n_kv; ap.d = head_dim; ap.out = out;
+  ap.ws = workspace; ap.ws_bytes = workspace ? workspace_bytes : 0;
   HIP_TRY(launch_attention(ap, dtype, (hipStream_t)hip_stream), "attention launch");
   return ORCH_OK;
 }

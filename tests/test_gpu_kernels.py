@@ -144,7 +144,7 @@ def test_qkv_scatter(orch_lib, dtype, H, heads, n_tok, kv_tokens, off):
 # ---- attention over fresh + stale K/V --------------------------------------
 
 def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fresh, seed,
-                    sample_rows=None):
+                    sample_rows=None, split=True):
     H = heads * d
     R = int(np.sqrt(n_kv))
     hdr = {"hidden": H, "heads": heads, "grid": R}
@@ -159,9 +159,11 @@ def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fres
     stale = np.concatenate([dit.kv_to_buffer_layout(hdr, Ks[b], Vs[b]) for b in range(B)])
     fresh = np.concatenate([dit.kv_to_buffer_layout(hdr, Kf[b], Vf[b]) for b in range(B)])
     out = empty((B, n_q, H), dtype)
+    wsb = orch_lib.attention_workspace_bytes(B, heads, n_q, n_kv, d, code(dtype)) if split else 0
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV) if wsb else None
     orch_lib.attention(qd, to_dev(stale, dtype), 2 * n_kv * H, to_dev(fresh, dtype),
                        2 * max(n_fresh, 1) * H, fresh_begin, n_fresh, B, heads, n_q, n_kv, d, out,
-                       code(dtype))
+                       code(dtype), workspace=ws)
     got = to_host(out)
     rows = np.arange(n_q) if sample_rows is None else sample_rows
     errs = []
@@ -187,6 +189,16 @@ def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fres
 def test_attention(orch_lib, dtype, heads, d, n_q, n_kv, fb, nf):
     err = _attention_case(orch_lib, dtype, 2, heads, d, n_q, n_kv, fb, nf, seed=n_q + n_kv + d)
     assert err <= (1e-5 if dtype == "f32" else 1e-2), err
+
+
+@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("n_q,n_kv,fb,nf", [(384, 4096, 1920, 384), (96, 1024, 512, 96),
+                                            (384, 1024, 0, 0)])
+def test_attention_split_keys(orch_lib, split, n_q, n_kv, fb, nf):
+    """Short bands split the keys over more workgroups (partials + combine)."""
+    assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, 72, 1) > 0
+    err = _attention_case(orch_lib, "bf16", 2, 16, 72, n_q, n_kv, fb, nf, seed=n_q + 1, split=split)
+    assert err <= 1e-2, err
 
 
 def test_attention_full_xl_shape_sampled(orch_lib):
