@@ -10,14 +10,15 @@ classifier-free guidance batch 2, and the scheduler update, at the first
 post-warm-up step t 780 -> 760 of the 50-step schedule.  Inputs are seeded
 and synthetic: random N(0, 0.02) weights, N(0, 1) latent, and a seeded
 stale K/V buffer with the spread of the model's K/V (0.02 sqrt(H)).  Every
-hot kernel is launched only at this band's shapes (the per-kernel split uses
-the same kernels and shapes through the kernel-level entry points), so a
-profiler's per-kernel averages over the run match the figures printed here;
---sweep adds the share sweep (other shapes).
+hot kernel is launched only at this band's shapes (the per-kernel split times
+the step's own launches), so a profiler's per-kernel averages over the run
+match the figures printed here; --sweep adds the share sweep (other shapes).
 
 Prints one JSON line: algorithmic TFLOP/s of the step (value), ms per step,
-the per-kernel split with the dominant kernel's roofline, the share sweep,
-and the CPU oracle timed on a bounded sample.
+the per-kernel split measured inside the steps (HIP events around every
+launch, a second pass after the timed one) with the dominant kernel's
+roofline, optionally the share sweep, and the CPU oracle timed on a bounded
+sample.
 """
 from __future__ import annotations
 
@@ -106,6 +107,40 @@ def kernel_split(torch, L, cfg, n_q: int, iters: int):
     return out
 
 
+def step_kernel_split(ctx, cfg, n_q: int, run_step, steps: int):
+    """Per-kernel-class average launch time inside the step itself: every
+    launch of `steps` steps bracketed by HIP events on the step's stream
+    (orch_set_kernel_timing), with the algorithmic work of one launch."""
+    H, F, B, N, L = cfg.hidden, cfg.mlp_hidden, cfg.cfg_batch, cfg.n_kv, cfg.n_blocks
+    M = B * n_q
+    flops = {"qkv_gemm": 2.0 * M * H * 3 * H, "attention": 4.0 * B * n_q * N * H,
+             "proj_gemm": 2.0 * M * H * H, "fc1_gemm": 2.0 * M * H * F, "fc2_gemm": 2.0 * M * F * H}
+    nbytes = {"layernorm": 6.0 * M * H,                       # fp32 in, bf16 out
+              "conditioning": 2.0 * (6 * H * H * L + 2 * H * H),  # adaLN weights streamed
+              "update": 16.0 * cfg.in_ch * (n_q // cfg.R) * cfg.patch * cfg.latent}
+    ctx.set_kernel_timing(True)
+    ctx.kernel_times()
+    for _ in range(steps):
+        run_step()
+    times = ctx.kernel_times()
+    ctx.set_kernel_timing(False)
+    out = {}
+    for k, (ms, n) in times.items():
+        if n == 0:
+            continue
+        avg = ms / n
+        rec = {"ms": round(avg, 5), "launches_per_step": n // steps,
+               "ms_per_step": round(ms / steps, 4)}
+        if k in flops:
+            rec["tflops"] = round(flops[k] / avg / 1e9, 1)
+            rec["flop_per_launch"] = flops[k]
+        if k in nbytes:
+            rec["gbs"] = round(nbytes[k] / avg / 1e6, 1)
+            rec["bytes_per_launch"] = nbytes[k]
+        out[k] = rec
+    return out
+
+
 def cpu_baseline(cfg, blob, x, labels, stale, rb, re, t, tp, blocks: int):
     """The oracle (float64 numpy) on the same band, truncated to `blocks`
     DiT blocks; rate scaled to the metric's unit by the sample's FLOPs."""
@@ -137,6 +172,46 @@ def cpu_baseline(cfg, blob, x, labels, stale, rb, re, t, tp, blocks: int):
             "ms_per_full_step_extrapolated": round(step_flops(cfg, (re - rb) * cfg.R) / (fl / dt) * 1e3, 1)}
 
 
+def run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q) -> int:
+    """Every executed step of the band's sampler (tiered for configs that use
+    it: Algorithm 1's reduced tier, Eq. (2)); x of the band is carried from
+    step to step and the buffer refreshed on executed steps."""
+    import torch
+
+    from paper_2509_04719_amd import schedule as psched
+    steps = (psched.tiered_schedule(cfg.T, cfg.steps, cfg.warmup) if cfg.tiered
+             else psched.plain_schedule(cfg.T, cfg.steps))
+    p = cfg.patch
+    out = torch.empty((cfg.in_ch, rows * p, cfg.latent), device=x.device)
+    total_flops = step_flops(cfg, n_q) * len(steps)
+
+    def sampler():
+        for st in steps:
+            ctx.step(x, 0, rows, st.t, st.t_prev, labels, cfg.cfg_scale, kv, int(st.refresh), out)
+            x[:, 0:rows * p].copy_(out)
+
+    sampler()                                          # warm-up pass
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(a.steps):
+        sampler()
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / a.steps
+    res = {"metric": "full-schedule ms of one device's band sampler", "value": round(ms, 3),
+           "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": 1,
+           "ms_per_step": round(ms / len(steps), 4), "higher_is_better": False,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": f"{cfg.name}: band {rows}/{cfg.R} rows, {len(steps)} executed "
+                                  f"steps ({'tiered: warm-up ' + str(cfg.warmup) + ', then stride 2' if cfg.tiered else 'plain'})",
+                      "executed_steps": len(steps), "n_q": n_q, "kv_len": cfg.n_kv},
+           "tflops": round(total_flops / ms / 1e9, 1)}
+    print(json.dumps(res), flush=True)
+    ctx.close()
+    return 0
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -145,9 +220,14 @@ def main(argv=None) -> int:
     ap.add_argument("--config", default="dit_xl2_1024")
     ap.add_argument("--share", type=float, default=0.40)
     ap.add_argument("--kernel-iters", type=int, default=20)
+    ap.add_argument("--op-split", action="store_true",
+                    help="also time each hot kernel alone through the kernel-level entry points")
     ap.add_argument("--cpu-blocks", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true", help="also time the share sweep")
+    ap.add_argument("--schedule", action="store_true",
+                    help="time the whole sampler schedule of the band instead of one step "
+                         "(the tiered schedule for configs that use it)")
     a = ap.parse_args(argv)
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -185,6 +265,9 @@ def main(argv=None) -> int:
     def one():
         ctx.step(x, rb, re, t, tp, labels, cfg.cfg_scale, kv, 1, out)
 
+    if a.schedule:
+        return run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q)
+
     for _ in range(a.warmup):
         one()
     torch.cuda.synchronize()
@@ -201,17 +284,20 @@ def main(argv=None) -> int:
     tflops = flops / ms / 1e9
     print(f"# step {ms:.3f} ms (median {float(np.median(per)):.3f}), {tflops:.1f} TFLOP/s", flush=True)
 
-    split = kernel_split(torch, L, cfg, n_q, a.kernel_iters)
-    per_step = {k: v["ms"] * cfg.n_blocks for k, v in split.items()}
-    dom = max(per_step, key=per_step.get)
+    split = step_kernel_split(ctx, cfg, n_q, one, a.steps)
+    dom = max(split, key=lambda k: split[k]["ms_per_step"])
     d = split[dom]
-    mfma_names = ["qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm"]
-    mfma_flops = sum(split[k]["flop_per_launch"] for k in mfma_names)
-    mfma_ms = sum(split[k]["ms"] for k in mfma_names)
+    mfma_names = [k for k in ("qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm") if k in split]
+    mfma_flops = sum(split[k]["flop_per_launch"] * split[k]["launches_per_step"] for k in mfma_names)
+    mfma_ms = sum(split[k]["ms_per_step"] for k in mfma_names)
     roofline = {"kernel": dom, "bound": "mfma", "achieved": d["tflops"], "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(d["tflops"] / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                "flop_per_launch": d["flop_per_launch"], "ms_per_launch": d["ms"]}
+                "flop_per_launch": d["flop_per_launch"], "ms_per_launch": d["ms"],
+                "measured": "HIP events around each launch inside the timed steps"}
     print(f"# kernels: {json.dumps(split)}", flush=True)
+    if a.op_split:
+        print(f"# kernel-level entry points: {json.dumps(kernel_split(torch, L, cfg, n_q, a.kernel_iters))}",
+              flush=True)
 
     sweep = {}
     if a.sweep:
@@ -242,6 +328,7 @@ def main(argv=None) -> int:
         "step_ms_median": round(float(np.median(per)), 4),
         "step_ms_p10_p90": [round(float(np.percentile(per, 10)), 4), round(float(np.percentile(per, 90)), 4)],
         "attn_gemm_tflops": round(mfma_flops / mfma_ms / 1e9, 1),
+        "attn_gemm_ms_per_step": round(mfma_ms, 4),
         "attn_gemm_frac": round(mfma_flops / mfma_ms / 1e9 / PEAK_BF16_TFLOPS, 4),
         "roofline": roofline,
         "kernels": split,

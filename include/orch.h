@@ -127,6 +127,22 @@ int orch_schedule_coefficients(const orch_dit_config* cfg, int t, int t_prev, do
 /* Thread-local message describing the last error ("" if none). */
 const char* orch_last_error(void);
 
+/* ---- per-kernel timing (measurement) -------------------------------------
+ * When enabled, every kernel launch of orch_patch_denoise_step is bracketed
+ * by a pair of HIP events on the caller's stream (the kernels themselves are
+ * unchanged).  orch_kernel_times synchronises on the recorded events, adds
+ * their elapsed times per kernel class into total_ms[class] and the launch
+ * counts into launches[class] (arrays of ORCH_KCLASS_COUNT entries, may be
+ * NULL), and clears the record.  Enabling allocates the event pool; disabling
+ * releases it. */
+enum {
+  ORCH_KCLASS_CONDITIONING = 0, ORCH_KCLASS_PATCH_EMBED, ORCH_KCLASS_LAYERNORM,
+  ORCH_KCLASS_QKV, ORCH_KCLASS_ATTENTION, ORCH_KCLASS_PROJ, ORCH_KCLASS_FC1,
+  ORCH_KCLASS_FC2, ORCH_KCLASS_FINAL, ORCH_KCLASS_UPDATE, ORCH_KCLASS_COUNT
+};
+int orch_set_kernel_timing(orch_ctx* ctx, int enable);
+int orch_kernel_times(orch_ctx* ctx, double* total_ms, long long* launches);
+
 /* ---- kernel-level entry points ------------------------------------------
  * The kernels of the step, callable one at a time on caller buffers (same
  * launch configuration the step uses).  `dtype` is ORCH_F32 or ORCH_BF16 and

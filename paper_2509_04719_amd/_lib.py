@@ -23,8 +23,10 @@ SYMBOLS = (
     "orch_patch_denoise_step", "orch_scheduler_update", "orch_schedule_coefficients",
     "orch_last_error", "orch_op_layernorm_modulate", "orch_op_linear", "orch_op_qkv_projection",
     "orch_op_attention", "orch_op_conditioning", "orch_op_patch_embed", "orch_op_final_layer",
-    "orch_attention_workspace_bytes",
+    "orch_attention_workspace_bytes", "orch_set_kernel_timing", "orch_kernel_times",
 )
+KCLASSES = ("conditioning", "patch_embed", "layernorm", "qkv_gemm", "attention", "proj_gemm",
+            "fc1_gemm", "fc2_gemm", "final_layer", "update")
 
 
 class OrchError(RuntimeError):
@@ -69,6 +71,8 @@ def _load():
         "orch_op_qkv_projection": (i, [vp, i, i, i, vp, vp, i, i, vp, vp, sz, i, i, i, vp]),
         "orch_op_attention": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, vp, sz, i, vp]),
         "orch_attention_workspace_bytes": (sz, [i, i, i, i, i, i]),
+        "orch_set_kernel_timing": (i, [vp, i]),
+        "orch_kernel_times": (i, [vp, C.POINTER(d), C.POINTER(C.c_longlong)]),
         "orch_op_conditioning": (i, [vp, i, C.POINTER(i), vp, vp]),
         "orch_op_patch_embed": (i, [vp, vp, i, i, vp, vp]),
         "orch_op_final_layer": (i, [vp, vp, i, i, vp, vp, vp]),
@@ -146,6 +150,16 @@ class DiTStep:
                                           lab, float(cfg_scale), _ptr(stale_kv), int(refresh),
                                           _ptr(z), float(eta), _ptr(out_eps), _ptr(out_x),
                                           _stream(stream)))
+
+    def set_kernel_timing(self, enable: bool):
+        check(lib.orch_set_kernel_timing(self.handle, int(enable)))
+
+    def kernel_times(self):
+        """{class: (total_ms, launches)} since the last call (synchronises)."""
+        ms = (C.c_double * len(KCLASSES))()
+        n = (C.c_longlong * len(KCLASSES))()
+        check(lib.orch_kernel_times(self.handle, ms, n))
+        return {k: (ms[i], n[i]) for i, k in enumerate(KCLASSES)}
 
     def conditioning(self, t, labels, out, stream=None):
         lab = (C.c_int * len(labels))(*[int(v) for v in labels])

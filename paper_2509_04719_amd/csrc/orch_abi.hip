@@ -88,6 +88,16 @@ struct orch_ctx {
   float* eps = nullptr;
   void* attn_ws = nullptr;
   size_t attn_ws_bytes = 0;
+
+  // per-kernel timing: event pairs recorded around each launch of a step
+  struct Timing {
+    bool on = false;
+    std::vector<hipEvent_t> ev;   // 2 per record
+    std::vector<int> cls;
+    size_t used = 0;
+    double ms[ORCH_KCLASS_COUNT] = {};
+    long long n[ORCH_KCLASS_COUNT] = {};
+  } timing;
 };
 
 namespace {
@@ -246,6 +256,7 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
 
 void orch_destroy(orch_ctx* x) {
   if (!x) return;
+  for (hipEvent_t e : x->timing.ev) (void)hipEventDestroy(e);
   if (x->ws) (void)hipFree(x->ws);
   if (x->wbuf) (void)hipFree(x->wbuf);
   if (x->fbuf) (void)hipFree(x->fbuf);
@@ -409,6 +420,43 @@ int check_labels(const orch_ctx* x, const int* labels) {
   return ORCH_OK;
 }
 
+constexpr size_t kTimingRecords = 8192;
+
+// Fold the recorded event pairs into the per-class sums (synchronises).
+int timing_flush(orch_ctx* x) {
+  auto& T = x->timing;
+  if (!T.used) return ORCH_OK;
+  HIP_TRY(hipEventSynchronize(T.ev[2 * T.used - 1]), "hipEventSynchronize");
+  for (size_t i = 0; i < T.used; ++i) {
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, T.ev[2 * i], T.ev[2 * i + 1]), "hipEventElapsedTime");
+    T.ms[T.cls[i]] += ms;
+    T.n[T.cls[i]] += 1;
+  }
+  T.used = 0;
+  return ORCH_OK;
+}
+
+// Record the start / stop of one launch of class `c` (no-op when off).
+struct KernelTimer {
+  orch_ctx* x;
+  hipStream_t s;
+  int c;
+  bool active = false;
+  KernelTimer(orch_ctx* x_, int c_, hipStream_t s_) : x(x_), s(s_), c(c_) {
+    auto& T = x->timing;
+    if (!T.on) return;
+    if (T.used == kTimingRecords && timing_flush(x) != ORCH_OK) return;
+    if (hipEventRecord(T.ev[2 * T.used], s) != hipSuccess) return;
+    active = true;
+  }
+  ~KernelTimer() {
+    if (!active) return;
+    auto& T = x->timing;
+    if (hipEventRecord(T.ev[2 * T.used + 1], s) == hipSuccess) T.cls[T.used++] = c;
+  }
+};
+
 int run_conditioning(orch_ctx* x, int t, const int* labels, float* mod, hipStream_t s) {
   CondParams cp{};
   cp.w_t1 = x->w_t1; cp.b_t1 = x->b_t1; cp.w_t2 = x->w_t2; cp.b_t2 = x->b_t2;
@@ -418,6 +466,7 @@ int run_conditioning(orch_ctx* x, int t, const int* labels, float* mod, hipStrea
   cp.labels[1] = x->B > 1 ? labels[1] : 0;
   cp.t = (float)t;
   cp.t1 = x->t1; cp.sc = x->sc; cp.mod = mod;
+  KernelTimer kt(x, ORCH_KCLASS_CONDITIONING, s);
   HIP_TRY(launch_conditioning(cp, x->cfg.dtype, s), "conditioning launch");
   return ORCH_OK;
 }
@@ -427,6 +476,7 @@ int run_patch_embed(orch_ctx* x, const float* x_full, int rb, int re, float* out
   pp.x = x_full; pp.w = x->w_pe; pp.b = x->b_pe; pp.pos = x->pos; pp.h = out;
   pp.C = x->cfg.in_ch; pp.latent = x->cfg.latent; pp.patch = x->cfg.patch; pp.grid = x->R;
   pp.hidden = x->H; pp.row_begin = rb; pp.n_rows = re - rb; pp.B = x->B;
+  KernelTimer kt(x, ORCH_KCLASS_PATCH_EMBED, s);
   HIP_TRY(launch_patch_embed(pp, s), "patch-embed launch");
   return ORCH_OK;
 }
@@ -435,12 +485,16 @@ int run_final(orch_ctx* x, const float* h, int rb, int re, const float* mod, flo
   const int n_tok = (re - rb) * x->R;
   const int dt = x->cfg.dtype;
   const float* shift = mod + (size_t)6 * x->H * x->L;
-  HIP_TRY(launch_layernorm_modulate(h, x->B * n_tok, x->H, n_tok, shift, shift + x->H, x->n_mod,
-                                    x->u, dt, s), "final LN launch");
+  {
+    KernelTimer kt(x, ORCH_KCLASS_LAYERNORM, s);
+    HIP_TRY(launch_layernorm_modulate(h, x->B * n_tok, x->H, n_tok, shift, shift + x->H,
+                                      x->n_mod, x->u, dt, s), "final LN launch");
+  }
   FinalParams fp{};
   fp.u = x->u; fp.w = x->w_final; fp.b = x->b_final; fp.eps = eps;
   fp.B = x->B; fp.n_tok = n_tok; fp.hidden = x->H; fp.out_ch = x->cfg.out_ch;
   fp.patch = x->cfg.patch; fp.grid = x->R; fp.n_rows = re - rb;
+  KernelTimer kt(x, ORCH_KCLASS_FINAL, s);
   HIP_TRY(launch_final_linear(fp, dt, s), "final linear launch");
   return ORCH_OK;
 }
@@ -506,7 +560,10 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
     const float* mb = x->mod + (size_t)6 * H * l;  // shift1 scale1 gate1 shift2 scale2 gate2
     void* layer_kv = (char*)stale_kv + (size_t)l * B * stale_bs * es;
 
-    HIP_TRY(launch_layernorm_modulate(x->h, M, H, n_tok, mb, mb + H, x->n_mod, x->u, dt, s), "LN1 launch");
+    {
+      KernelTimer kt(x, ORCH_KCLASS_LAYERNORM, s);
+      HIP_TRY(launch_layernorm_modulate(x->h, M, H, n_tok, mb, mb + H, x->n_mod, x->u, dt, s), "LN1 launch");
+    }
 
     EpiParams eq{};
     eq.bias = x->b_qkv[l];
@@ -518,7 +575,10 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
     } else {
       eq.kv = x->kvf; eq.kv_branch_stride = fresh_bs; eq.kv_tokens = n_tok; eq.tok_offset = 0;
     }
-    HIP_TRY(launch_gemm(x->u, x->w_qkv[l], M, 3 * H, H, kEpiQkv, eq, dt, s), "QKV launch");
+    {
+      KernelTimer kt(x, ORCH_KCLASS_QKV, s);
+      HIP_TRY(launch_gemm(x->u, x->w_qkv[l], M, 3 * H, H, kEpiQkv, eq, dt, s), "QKV launch");
+    }
 
     AttnParams ap{};
     ap.q = x->q; ap.kv_stale = layer_kv; ap.stale_bs = stale_bs;
@@ -526,23 +586,38 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
     ap.fresh_begin = refresh ? 0 : rb * x->R; ap.n_fresh = refresh ? 0 : n_tok;
     ap.B = B; ap.heads = x->heads; ap.n_q = n_tok; ap.n_kv = x->n_kv; ap.d = x->d; ap.out = x->att;
     ap.ws = x->attn_ws; ap.ws_bytes = x->attn_ws_bytes;
-    HIP_TRY(launch_attention(ap, dt, s), "attention launch");
+    {
+      KernelTimer kt(x, ORCH_KCLASS_ATTENTION, s);
+      HIP_TRY(launch_attention(ap, dt, s), "attention launch");
+    }
 
     EpiParams eo{};
     eo.out = x->h; eo.bias = x->b_proj[l]; eo.gate = mb + 2 * H; eo.gate_stride = x->n_mod;
     eo.rows_per_batch = n_tok;
-    HIP_TRY(launch_gemm(x->att, x->w_proj[l], M, H, H, kEpiResidual, eo, dt, s), "proj launch");
+    {
+      KernelTimer kt(x, ORCH_KCLASS_PROJ, s);
+      HIP_TRY(launch_gemm(x->att, x->w_proj[l], M, H, H, kEpiResidual, eo, dt, s), "proj launch");
+    }
 
-    HIP_TRY(launch_layernorm_modulate(x->h, M, H, n_tok, mb + 3 * H, mb + 4 * H, x->n_mod, x->u, dt, s), "LN2 launch");
+    {
+      KernelTimer kt(x, ORCH_KCLASS_LAYERNORM, s);
+      HIP_TRY(launch_layernorm_modulate(x->h, M, H, n_tok, mb + 3 * H, mb + 4 * H, x->n_mod, x->u, dt, s), "LN2 launch");
+    }
 
     EpiParams e1{};
     e1.out = x->mlp; e1.bias = x->b_fc1[l];
-    HIP_TRY(launch_gemm(x->u, x->w_fc1[l], M, F, H, kEpiGelu, e1, dt, s), "fc1 launch");
+    {
+      KernelTimer kt(x, ORCH_KCLASS_FC1, s);
+      HIP_TRY(launch_gemm(x->u, x->w_fc1[l], M, F, H, kEpiGelu, e1, dt, s), "fc1 launch");
+    }
 
     EpiParams e2{};
     e2.out = x->h; e2.bias = x->b_fc2[l]; e2.gate = mb + 5 * H; e2.gate_stride = x->n_mod;
     e2.rows_per_batch = n_tok;
-    HIP_TRY(launch_gemm(x->mlp, x->w_fc2[l], M, H, F, kEpiResidual, e2, dt, s), "fc2 launch");
+    {
+      KernelTimer kt(x, ORCH_KCLASS_FC2, s);
+      HIP_TRY(launch_gemm(x->mlp, x->w_fc2[l], M, H, F, kEpiResidual, e2, dt, s), "fc2 launch");
+    }
   }
 
   float* eps = out_eps ? out_eps : x->eps;
@@ -554,9 +629,13 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
   const float* zb = z ? z + (size_t)rb * p * c.latent : nullptr;
   const float* ec = eps;
   const float* eu = B > 1 ? eps + (size_t)c.out_ch * band_cols : nullptr;
-  HIP_TRY(launch_update(xb, (int)lat2, ec, eu, cfg_scale, abc[2] != 0.0 ? zb : nullptr, (int)lat2,
-                        (float)abc[0], (float)abc[1], (float)abc[2], out_x_patch, c.in_ch, band_cols, s),
-          "update launch");
+  {
+    KernelTimer kt(x, ORCH_KCLASS_UPDATE, s);
+    HIP_TRY(launch_update(xb, (int)lat2, ec, eu, cfg_scale, abc[2] != 0.0 ? zb : nullptr, (int)lat2,
+                          (float)abc[0], (float)abc[1], (float)abc[2], out_x_patch, c.in_ch,
+                          band_cols, s),
+            "update launch");
+  }
   return ORCH_OK;
 }
 
@@ -686,6 +765,49 @@ int orch_op_final_layer(orch_ctx* x, const float* h, int rb, int re, const float
   int rc = check_device(x);
   if (rc) return rc;
   return run_final(x, h, rb, re, mod, out_eps, (hipStream_t)hip_stream);
+}
+
+int orch_set_kernel_timing(orch_ctx* x, int enable) {
+  if (!x) return fail(ORCH_EINVAL, "ctx is NULL");
+  auto& T = x->timing;
+  if (enable && !T.on) {
+    T.ev.assign(2 * kTimingRecords, nullptr);
+    for (auto& e : T.ev) {
+      hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) {
+        for (hipEvent_t f : T.ev)
+          if (f) (void)hipEventDestroy(f);
+        T.ev.clear();
+        return hip_fail(r, "hipEventCreate");
+      }
+    }
+    T.cls.assign(kTimingRecords, 0);
+    T.used = 0;
+    for (int i = 0; i < ORCH_KCLASS_COUNT; ++i) { T.ms[i] = 0.0; T.n[i] = 0; }
+    T.on = true;
+  } else if (!enable && T.on) {
+    int rc = timing_flush(x);
+    for (hipEvent_t e : T.ev) (void)hipEventDestroy(e);
+    T.ev.clear();
+    T.cls.clear();
+    T.on = false;
+    if (rc) return rc;
+  }
+  return ORCH_OK;
+}
+
+int orch_kernel_times(orch_ctx* x, double* total_ms, long long* launches) {
+  if (!x) return fail(ORCH_EINVAL, "ctx is NULL");
+  auto& T = x->timing;
+  int rc = timing_flush(x);
+  if (rc) return rc;
+  for (int i = 0; i < ORCH_KCLASS_COUNT; ++i) {
+    if (total_ms) total_ms[i] = T.ms[i];
+    if (launches) launches[i] = T.n[i];
+    T.ms[i] = 0.0;
+    T.n[i] = 0;
+  }
+  return ORCH_OK;
 }
 
 }  // extern "C"

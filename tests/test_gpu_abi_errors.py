@@ -100,3 +100,27 @@ def test_op_argument_checks(orch_lib):
         orch_lib.attention(a, a, 16, None, 0, 0, 4, 1, 1, 4, 64, 32, a, 0)  # fresh without pointer
     with pytest.raises(orch_lib.OrchError):
         orch_lib.scheduler_update(a, a, None, 1.5, None, 1.0, 0.5, 0.3, a)  # c != 0 without z
+
+
+def test_kernel_timing_counts(orch_lib, setup):
+    """Per-kernel timing records every launch of the step by class and does
+    not change its result."""
+    ctx, _, x, kv = setup
+    out0 = empty((CFG.in_ch, 8, CFG.latent))
+    out1 = empty((CFG.in_ch, 8, CFG.latent))
+    assert _step(orch_lib, ctx, x, kv, out0) == orch_lib.ORCH_OK
+    ctx.set_kernel_timing(True)
+    for _ in range(3):
+        assert _step(orch_lib, ctx, x, kv, out1) == orch_lib.ORCH_OK
+    t = ctx.kernel_times()
+    ctx.set_kernel_timing(False)
+    L = CFG.n_blocks
+    want = {"conditioning": 1, "patch_embed": 1, "layernorm": 2 * L + 1, "qkv_gemm": L,
+            "attention": L, "proj_gemm": L, "fc1_gemm": L, "fc2_gemm": L, "final_layer": 1,
+            "update": 1}
+    for k, n in want.items():
+        assert t[k][1] == 3 * n, (k, t[k])
+        assert t[k][0] > 0.0
+    torch.cuda.synchronize()
+    assert torch.equal(out0, out1)
+    assert all(v == (0.0, 0) for v in ctx.kernel_times().values())
