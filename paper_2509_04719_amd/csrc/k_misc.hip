@@ -14,7 +14,14 @@ namespace orch {
 
 // ---------------------------------------------------------------------------
 // adaLN LayerNorm: one wave per row, the row held in registers as float2
-// (hidden % 128 == 0, hidden <= 2048), two-pass mean / variance in fp32.
+// (hidden % 128 == 0, hidden <= 2048).  The statistics are shifted sums
+// sum(x - x0), sum((x - x0)^2) with x0 the row's first element (stable
+// against a large mean), reduced together in one pass; shift and scale are
+// loaded with the row, and the output is written as packed pairs.
+template <typename T> struct Pair;
+template <> struct Pair<float> { typedef float type __attribute__((ext_vector_type(2))); };
+template <> struct Pair<bf16> { typedef __bf16 type __attribute__((ext_vector_type(2))); };
+
 template <typename T>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x, int rows, int H,
                                                      int rpb, const float* __restrict__ shift,
@@ -24,36 +31,117 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
   const int nv = H >> 7;
+  const int b = row / rpb;
   const float2* xr = reinterpret_cast<const float2*>(x + (size_t)row * H);
-  float2 v[16];
-  float s = 0.0f;
+  const float2* shr = reinterpret_cast<const float2*>(shift + (size_t)b * mod_stride);
+  const float2* scr = reinterpret_cast<const float2*>(scale + (size_t)b * mod_stride);
+  float2 v[16], sh[16], sc[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i)
     if (i < nv) {
       v[i] = xr[lane + 64 * i];
-      s += v[i].x + v[i].y;
+      sh[i] = shr[lane + 64 * i];
+      sc[i] = scr[lane + 64 * i];
     }
-  const float mean = wave_sum(s) / (float)H;
-  float s2 = 0.0f;
+  const float x0 = __shfl(v[0].x, 0, kWave);
+  float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i)
     if (i < nv) {
-      const float a = v[i].x - mean, c = v[i].y - mean;
+      const float a = v[i].x - x0, c = v[i].y - x0;
+      s1 += a + c;
       s2 += a * a + c * c;
     }
-  const float var = wave_sum(s2) / (float)H;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    s1 += __shfl_xor(s1, o, kWave);
+    s2 += __shfl_xor(s2, o, kWave);
+  }
+  const float inv_h = 1.0f / (float)H;
+  const float dmean = s1 * inv_h;
+  const float var = fmaxf(s2 * inv_h - dmean * dmean, 0.0f);
+  const float mean = x0 + dmean;
   const float rstd = 1.0f / sqrtf(var + 1e-6f);
-  const int b = row / rpb;
-  const float* sh = shift + (size_t)b * mod_stride;
-  const float* sc = scale + (size_t)b * mod_stride;
-  T* o = out + (size_t)row * H;
+  typedef typename Pair<T>::type P;
+  P* o = reinterpret_cast<P*>(out + (size_t)row * H);
 #pragma unroll
   for (int i = 0; i < 16; ++i)
     if (i < nv) {
-      const int col = 2 * (lane + 64 * i);
-      o[col] = from_f<T>((v[i].x - mean) * rstd * (1.0f + sc[col]) + sh[col]);
-      o[col + 1] = from_f<T>((v[i].y - mean) * rstd * (1.0f + sc[col + 1]) + sh[col + 1]);
+      P w;
+      w[0] = from_f<T>((v[i].x - mean) * rstd * (1.0f + sc[i].x) + sh[i].x);
+      w[1] = from_f<T>((v[i].y - mean) * rstd * (1.0f + sc[i].y) + sh[i].y);
+      o[lane + 64 * i] = w;
     }
+}
+
+// The same for a compile-time row length: two rows per wave (32 lanes each),
+// 16-byte loads, NV float4 per lane (H = 128 NV).
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void ln_mod_fixed_kernel(const float* __restrict__ x, int rows,
+                                                           int rpb, const float* __restrict__ shift,
+                                                           const float* __restrict__ scale,
+                                                           int mod_stride, T* __restrict__ out) {
+  constexpr int H = 128 * NV;
+  const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
+  const int lane = threadIdx.x & 31;
+  if (row >= rows) return;
+  const int b = row / rpb;
+  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)row * H);
+  const float4* shr = reinterpret_cast<const float4*>(shift + (size_t)b * mod_stride);
+  const float4* scr = reinterpret_cast<const float4*>(scale + (size_t)b * mod_stride);
+  float4 v[NV], sh[NV], sc[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = xr[lane + 32 * i];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    sh[i] = shr[lane + 32 * i];
+    sc[i] = scr[lane + 32 * i];
+  }
+  const float x0 = __shfl(v[0].x, 0, 32);
+  float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const float a = v[i].x - x0, c = v[i].y - x0, d = v[i].z - x0, e = v[i].w - x0;
+    s1 += (a + c) + (d + e);
+    s2 += (a * a + c * c) + (d * d + e * e);
+  }
+#pragma unroll
+  for (int o = 16; o > 0; o >>= 1) {
+    s1 += __shfl_xor(s1, o, 32);
+    s2 += __shfl_xor(s2, o, 32);
+  }
+  constexpr float inv_h = 1.0f / (float)H;
+  const float dmean = s1 * inv_h;
+  const float var = fmaxf(s2 * inv_h - dmean * dmean, 0.0f);
+  const float mean = x0 + dmean;
+  const float rstd = 1.0f / sqrtf(var + 1e-6f);
+  typedef T Q __attribute__((ext_vector_type(4)));
+  Q* o = reinterpret_cast<Q*>(out + (size_t)row * H);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    Q w;
+    w[0] = from_f<T>((v[i].x - mean) * rstd * (1.0f + sc[i].x) + sh[i].x);
+    w[1] = from_f<T>((v[i].y - mean) * rstd * (1.0f + sc[i].y) + sh[i].y);
+    w[2] = from_f<T>((v[i].z - mean) * rstd * (1.0f + sc[i].z) + sh[i].z);
+    w[3] = from_f<T>((v[i].w - mean) * rstd * (1.0f + sc[i].w) + sh[i].w);
+    o[lane + 32 * i] = w;
+  }
+}
+
+template <typename T>
+static void launch_ln_t(const float* x, int rows, int hidden, int rpb, const float* shift,
+                        const float* scale, int mod_stride, T* out, hipStream_t s) {
+  const bool al = ((uintptr_t)shift % 16 == 0) && ((uintptr_t)scale % 16 == 0) && mod_stride % 4 == 0;
+  if (al && hidden == 1152) {
+    hipLaunchKernelGGL((ln_mod_fixed_kernel<T, 9>), dim3(ceil_div(rows, 8)), dim3(256), 0, s, x,
+                       rows, rpb, shift, scale, mod_stride, out);
+  } else if (al && hidden == 384) {
+    hipLaunchKernelGGL((ln_mod_fixed_kernel<T, 3>), dim3(ceil_div(rows, 8)), dim3(256), 0, s, x,
+                       rows, rpb, shift, scale, mod_stride, out);
+  } else {
+    hipLaunchKernelGGL(ln_mod_kernel<T>, dim3(ceil_div(rows, 4)), dim3(256), 0, s, x, rows,
+                       hidden, rpb, shift, scale, mod_stride, out);
+  }
 }
 
 hipError_t launch_layernorm_modulate(const float* x, int rows, int hidden, int rpb,
@@ -61,13 +149,10 @@ hipError_t launch_layernorm_modulate(const float* x, int rows, int hidden, int r
                                      void* out, int dtype, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (hidden % 128 != 0 || hidden > 2048) return hipErrorInvalidValue;
-  dim3 grid(ceil_div(rows, 4));
   if (dtype == kBF16)
-    hipLaunchKernelGGL(ln_mod_kernel<bf16>, grid, dim3(256), 0, s, x, rows, hidden, rpb, shift,
-                       scale, mod_stride, reinterpret_cast<bf16*>(out));
+    launch_ln_t<bf16>(x, rows, hidden, rpb, shift, scale, mod_stride, reinterpret_cast<bf16*>(out), s);
   else
-    hipLaunchKernelGGL(ln_mod_kernel<float>, grid, dim3(256), 0, s, x, rows, hidden, rpb, shift,
-                       scale, mod_stride, reinterpret_cast<float*>(out));
+    launch_ln_t<float>(x, rows, hidden, rpb, shift, scale, mod_stride, reinterpret_cast<float*>(out), s);
   return hipGetLastError();
 }
 
@@ -116,8 +201,9 @@ __global__ __launch_bounds__(256) void temb2_kernel(const T* __restrict__ w2,
 
 // mod[b][n] = W_ada[n] . sc[b] + b_ada[n] for every adaLN row of every block:
 // streams the whole adaLN weight once.  Each lane keeps its 8-element slices
-// of sc in registers and the wave walks rows grid-stride.
-template <typename T>
+// of sc in registers; a wave takes RPW rows at a time (their loads in flight
+// together) and reduces the 2 * RPW dot products in one interleaved pass.
+template <typename T, int RPW>
 __global__ __launch_bounds__(256) void adaln_gemv_kernel(const T* __restrict__ w,
                                                          const float* __restrict__ bias,
                                                          const float* __restrict__ sc, int H,
@@ -137,36 +223,54 @@ __global__ __launch_bounds__(256) void adaln_gemv_kernel(const T* __restrict__ w
       xs[1][j][e] = (ck < nck && B > 1) ? sc[H + ck * 8 + e] : 0.0f;
     }
   }
-  for (int n = wave_id; n < n_rows; n += n_waves) {
-    const T* wr = w + (size_t)n * H;
-    float a0 = 0.0f, a1 = 0.0f;
+  for (int n0 = wave_id * RPW; n0 < n_rows; n0 += n_waves * RPW) {
+    float acc[RPW][2];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) acc[r][0] = acc[r][1] = 0.0f;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int ck = lane + 64 * j;
       if (ck < nck) {
-        float wv[8];
-        if constexpr (sizeof(T) == 2) {
-          const bf16x8 q = *reinterpret_cast<const bf16x8*>(wr + ck * 8);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) wv[e] = (float)q[e];
-        } else {
-          const float4 q0 = *reinterpret_cast<const float4*>(wr + ck * 8);
-          const float4 q1 = *reinterpret_cast<const float4*>(wr + ck * 8 + 4);
-          wv[0] = q0.x; wv[1] = q0.y; wv[2] = q0.z; wv[3] = q0.w;
-          wv[4] = q1.x; wv[5] = q1.y; wv[6] = q1.z; wv[7] = q1.w;
-        }
+        for (int r = 0; r < RPW; ++r) {
+          const int n = min(n0 + r, n_rows - 1);
+          const T* wr = w + (size_t)n * H + ck * 8;
+          float wv[8];
+          if constexpr (sizeof(T) == 2) {
+            const bf16x8 q = *reinterpret_cast<const bf16x8*>(wr);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          a0 = fmaf(wv[e], xs[0][j][e], a0);
-          a1 = fmaf(wv[e], xs[1][j][e], a1);
+            for (int e = 0; e < 8; ++e) wv[e] = (float)q[e];
+          } else {
+            const float4 q0 = *reinterpret_cast<const float4*>(wr);
+            const float4 q1 = *reinterpret_cast<const float4*>(wr + 4);
+            wv[0] = q0.x; wv[1] = q0.y; wv[2] = q0.z; wv[3] = q0.w;
+            wv[4] = q1.x; wv[5] = q1.y; wv[6] = q1.z; wv[7] = q1.w;
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            acc[r][0] = fmaf(wv[e], xs[0][j][e], acc[r][0]);
+            acc[r][1] = fmaf(wv[e], xs[1][j][e], acc[r][1]);
+          }
         }
       }
     }
-    a0 = wave_sum(a0);
-    if (B > 1) a1 = wave_sum(a1);
-    if (lane == 0) {
-      mod[n] = a0 + bias[n];
-      if (B > 1) mod[(size_t)n_rows + n] = a1 + bias[n];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+        acc[r][0] += __shfl_xor(acc[r][0], o, kWave);
+        acc[r][1] += __shfl_xor(acc[r][1], o, kWave);
+      }
+    if (lane < RPW) {
+      float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+      for (int r = 0; r < RPW; ++r)
+        if (r == lane) { a0 = acc[r][0]; a1 = acc[r][1]; }
+      const int n = n0 + lane;
+      if (n < n_rows) {
+        mod[n] = a0 + bias[n];
+        if (B > 1) mod[(size_t)n_rows + n] = a1 + bias[n];
+      }
     }
   }
 }
@@ -179,8 +283,9 @@ static hipError_t launch_cond_t(const CondParams& p, hipStream_t s) {
                      reinterpret_cast<const T*>(p.w_t2), p.b_t2, p.t1,
                      reinterpret_cast<const T*>(p.table), p.hidden, p.B, p.labels[0],
                      p.labels[1], p.sc);
-  const int blocks = min(2048, ceil_div(p.n_mod, 4));
-  hipLaunchKernelGGL(adaln_gemv_kernel<T>, dim3(blocks), dim3(256), 0, s,
+  constexpr int RPW = 4;
+  const int blocks = min(2048, ceil_div(p.n_mod, 4 * RPW));
+  hipLaunchKernelGGL((adaln_gemv_kernel<T, RPW>), dim3(blocks), dim3(256), 0, s,
                      reinterpret_cast<const T*>(p.w_ada), p.b_ada, p.sc, p.hidden, p.n_mod, p.B,
                      p.mod);
   return hipGetLastError();
@@ -193,32 +298,41 @@ hipError_t launch_conditioning(const CondParams& p, int dtype, hipStream_t s) {
 
 // ---------------------------------------------------------------------------
 // Patch embedding of the band: h[b][tok][n] = W[n] . patch(tok) + bias[n]
-// + pos[global tok][n], patch vector ordered (channel, dy, dx).
+// + pos[global tok][n], patch vector ordered (channel, dy, dx).  The weight is
+// held transposed, wt[k][n], so a block's threads read it coalesced.
+constexpr int kPatchTok = 4;  // tokens per thread
+
+// (patch 2, 4 channels: a 16-element patch vector, index k = c*4 + dy*2 + dx)
 __global__ __launch_bounds__(128) void patch_embed_kernel(PatchEmbedParams p) {
-  const int tok = blockIdx.x;                    // band-local token
   const int n = blockIdx.y * 128 + threadIdx.x;  // output feature
   if (n >= p.hidden) return;
-  const int i = tok / p.grid, j = tok - (tok / p.grid) * p.grid;
-  const int gi = p.row_begin + i;
-  const int pd = p.C * p.patch * p.patch;
-  const float* wr = p.w + (size_t)n * pd;
-  float acc = p.b[n];
-  int k = 0;
-  for (int c = 0; c < p.C; ++c)
-    for (int dy = 0; dy < p.patch; ++dy)
-      for (int dx = 0; dx < p.patch; ++dx, ++k) {
-        const float xv = p.x[((size_t)c * p.latent + gi * p.patch + dy) * p.latent + j * p.patch + dx];
-        acc = fmaf(wr[k], xv, acc);
-      }
-  acc += p.pos[((size_t)gi * p.grid + j) * p.hidden + n];
+  float wk[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) wk[k] = p.w[(size_t)k * p.hidden + n];
+  const float bias = p.b[n];
   const int n_tok = p.n_rows * p.grid;
-  for (int b = 0; b < p.B; ++b) p.h[((size_t)b * n_tok + tok) * p.hidden + n] = acc;
+  for (int u = 0; u < kPatchTok; ++u) {
+    const int tok = blockIdx.x * kPatchTok + u;    // band-local token
+    if (tok >= n_tok) break;
+    const int i = tok / p.grid, j = tok - (tok / p.grid) * p.grid;
+    const int gi = p.row_begin + i;
+    float acc = bias;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int c = k >> 2, dy = (k >> 1) & 1, dx = k & 1;
+      acc = fmaf(wk[k], p.x[((size_t)c * p.latent + gi * 2 + dy) * p.latent + j * 2 + dx], acc);
+    }
+    acc += p.pos[((size_t)gi * p.grid + j) * p.hidden + n];
+    for (int b = 0; b < p.B; ++b) p.h[((size_t)b * n_tok + tok) * p.hidden + n] = acc;
+  }
 }
 
 hipError_t launch_patch_embed(const PatchEmbedParams& p, hipStream_t s) {
   const int n_tok = p.n_rows * p.grid;
   if (n_tok <= 0) return hipSuccess;
-  hipLaunchKernelGGL(patch_embed_kernel, dim3(n_tok, ceil_div(p.hidden, 128)), dim3(128), 0, s, p);
+  if (p.patch != 2 || p.C != 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(patch_embed_kernel, dim3(ceil_div(n_tok, kPatchTok), ceil_div(p.hidden, 128)),
+                     dim3(128), 0, s, p);
   return hipGetLastError();
 }
 

@@ -79,7 +79,7 @@ hipError_t launch_conditioning(const CondParams& p, int dtype, hipStream_t strea
 
 struct PatchEmbedParams {
   const float* x;        // fp32 [C][latent][latent]
-  const float* w;        // fp32 [H][C*p*p]
+  const float* w;        // fp32 [C*p*p][H] (transposed)
   const float* b;        // fp32 [H]
   const float* pos;      // fp32 [N_kv][H]
   float* h;              // fp32 [B][n_tok][H]

@@ -112,8 +112,8 @@ int validate_config(const orch_dit_config* c) {
     return fail(ORCH_EINVAL, "head_dim %d not in {32,64,72,80,96,128}", d);
   if (c->hidden % 128 || c->hidden > 2048) return fail(ORCH_EINVAL, "hidden must be a multiple of 128, <= 2048");
   if (c->patch != 2) return fail(ORCH_EINVAL, "patch must be 2");
-  if (c->in_ch < 1 || c->out_ch * c->patch * c->patch != 16)
-    return fail(ORCH_EINVAL, "out_ch * patch^2 must be 16");
+  if (c->in_ch * c->patch * c->patch != 16 || c->out_ch * c->patch * c->patch != 16)
+    return fail(ORCH_EINVAL, "in_ch * patch^2 and out_ch * patch^2 must be 16");
   if (c->latent < c->patch || c->latent % c->patch) return fail(ORCH_EINVAL, "latent %% patch != 0");
   if (((c->latent / c->patch) * (c->latent / c->patch)) % 64)
     return fail(ORCH_EINVAL, "token count must be a multiple of 64");
@@ -350,7 +350,15 @@ int orch_load_dit_weights(orch_ctx* x, const void* host_blob, size_t nbytes) {
     to_f32(t, hf.data() + at);
     return at;
   };
-  const size_t f_pe_w = fadd(tab[0]);
+  // patch-embedding weight, stored transposed [C*p*p][H] for coalesced reads
+  const size_t f_pe_w = hf.size();
+  {
+    std::vector<float> wpe(tab[0].count);
+    to_f32(tab[0], wpe.data());
+    hf.resize(f_pe_w + (tab[0].count + 63) / 64 * 64);
+    for (size_t n = 0; n < H; ++n)
+      for (int k = 0; k < x->pdim; ++k) hf[f_pe_w + (size_t)k * H + n] = wpe[n * x->pdim + k];
+  }
   const size_t f_pe_b = fadd(tab[1]);
   const size_t f_pos = fadd(tab[2]);
   const size_t f_t1 = fadd(tab[4]);
