@@ -2,12 +2,11 @@
 // (plain store, GELU, gated residual add into the fp32 residual stream, and
 // the QKV scatter into the head-major Q buffer and the K / V^T buffer).
 //
-// bf16 path: BM x BN x 64 tiles, WM x WN waves, each wave a (BM/WM) x (BN/WN)
-// block of v_mfma_f32_32x32x16_bf16 with fp32 accumulation; operands staged
-// global -> registers -> padded LDS rows (144 B, conflict-free 16-byte reads),
-// double buffered, one barrier per k-tile.  fp32 path (and shapes the MFMA
-// tiling does not cover): a 64x64 SIMT tile with 4x4 outputs per thread.
+// bf16 path: MFMA tiles fed by direct-to-LDS loads (described at the kernel).
+// fp32 path (and shapes the MFMA tiling does not cover): a 64x64 SIMT tile
+// with 4x4 outputs per thread.
 #include <cstdlib>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -127,146 +126,186 @@ struct Epilogue {
 };
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA GEMM
-constexpr int kBK = 64;
-constexpr int kLdsStride = kBK + 8;  // bf16 per LDS row: 144 B
+// Epilogue of the MFMA GEMM.  The MFMAs produce transposed 32x32 blocks, so a
+// lane holds C[m][n..n+3] (m = lane % 32 of the block, n = 8g + 4(lane / 32)).
+// Each wave stages one 32-row strip of its tile at a time in a private LDS
+// area (row stride TN + 4 floats, so the 16-byte writes of 16 rows land in
+// distinct banks), then walks the strip in chunks along n: every global load
+// and store is 16 bytes wide and a row's chunks are contiguous.  The QKV
+// scatter writes Q and K rows the same way and walks V^T columns (8 tokens of
+// one channel per lane).
+template <int FM, int FN, int EPI>
+struct StripEpilogue {
+  static constexpr int TN = 32 * FN;
+  static constexpr int LS = TN + 4;
+  static constexpr int BYTES = 32 * LS * 4;  // LDS per wave
 
-template <int BM, int BN, int WM, int WN, int EPI>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_mfma_kernel(
-    const bf16* __restrict__ A, const bf16* __restrict__ W, int M, int N, int K, EpiParams ep) {
-  constexpr int NT = 64 * WM * WN;           // threads
-  constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
-  constexpr int FM = TM / 32, FN = TN / 32;  // 32x32 blocks per wave
-  constexpr int CH_A = BM * (kBK / 8);       // 16-byte chunks per tile
-  constexpr int CH_B = BN * (kBK / 8);
-  constexpr int LA = (CH_A + NT - 1) / NT;
-  constexpr int LB = (CH_B + NT - 1) / NT;
-  static_assert(CH_A % NT == 0 && CH_B % NT == 0, "tile must split evenly over threads");
+  const EpiParams& ep;
+  int M, N;
 
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * kLdsStride];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * kLdsStride];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int m0 = blockIdx.y * BM;
-  const int n0 = blockIdx.x * BN;
-
-  // this thread's global chunks: chunk c = tid + NT*i -> row c/8, k-chunk c%8
-  const bf16* pa[LA];
-  const bf16* pb[LB];
-  int la[LA], lb[LB];
-#pragma unroll
-  for (int i = 0; i < LA; ++i) {
-    const int c = tid + NT * i;
-    const int r = c >> 3, kc = c & 7;
-    pa[i] = A + (size_t)min(m0 + r, M - 1) * K + kc * 8;
-    la[i] = r * kLdsStride + kc * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < LB; ++i) {
-    const int c = tid + NT * i;
-    const int r = c >> 3, kc = c & 7;
-    pb[i] = W + (size_t)(n0 + r) * K + kc * 8;
-    lb[i] = r * kLdsStride + kc * 8;
+  __device__ __forceinline__ int branch_of(int m) const {
+    int b = 0;
+    while (m >= (b + 1) * ep.rows_per_batch) ++b;
+    return b;
   }
 
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  __device__ __forceinline__ static float act(float y) {
+    if (EPI != kEpiGelu) return y;
+    const float u = 0.7978845608028654f * (y + 0.044715f * y * y * y);
+    const float e = __expf(2.0f * u);
+    const float th = 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
+    return 0.5f * y * (1.0f + th);
+  }
 
-  const int KT = K / kBK;
-  uint4 ra[LA], rb[LB];
+  // rows [mr, mr + 32) x columns [n0, n0 + TN) of C, staged in strip
+  __device__ __forceinline__ void rows_store(const float* strip, int lane, int mr, int n0) const {
+    constexpr int CH = TN / 8, IT = 32 * CH / 64;
+    bf16* out = reinterpret_cast<bf16*>(ep.out);
 #pragma unroll
-  for (int i = 0; i < LA; ++i) ra[i] = *reinterpret_cast<const uint4*>(pa[i]);
+    for (int q = 0; q < IT; ++q) {
+      const int f = q * 64 + lane, row = f / CH, c = f % CH;
+      const int m = mr + row, n = n0 + c * 8;
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8);
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8 + 4);
+      if (m < M) {
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(ep.bias + n);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(ep.bias + n + 4);
+        bf16x8 o;
 #pragma unroll
-  for (int i = 0; i < LB; ++i) rb[i] = *reinterpret_cast<const uint4*>(pb[i]);
-#pragma unroll
-  for (int i = 0; i < LA; ++i) *reinterpret_cast<uint4*>(&sA[0][la[i]]) = ra[i];
-#pragma unroll
-  for (int i = 0; i < LB; ++i) *reinterpret_cast<uint4*>(&sB[0][lb[i]]) = rb[i];
-  __syncthreads();
+        for (int r = 0; r < 4; ++r) {
+          o[r] = from_f<bf16>(act(x0[r] + b0[r]));
+          o[4 + r] = from_f<bf16>(act(x1[r] + b1[r]));
+        }
+        *reinterpret_cast<bf16x8*>(out + (size_t)m * N + n) = o;
+      }
+    }
+  }
 
-  const int lrow = lane & 31;
-  const int lk = (lane >> 5) * 8;
-  const bf16* sa_base = &sA[0][(wm * TM + lrow) * kLdsStride + lk];
-  const bf16* sb_base = &sB[0][(wn * TN + lrow) * kLdsStride + lk];
+  __device__ __forceinline__ void rows_residual(const float* strip, int lane, int mr, int n0) const {
+    constexpr int CH = TN / 4, IT = 32 * CH / 64;
+    float* hb = reinterpret_cast<float*>(ep.out);
+    f32x4 x[IT], hv[IT];
+    // all loads first: the stores below may alias them as far as the
+    // compiler knows, so this keeps one round trip per strip
+#pragma unroll
+    for (int q = 0; q < IT; ++q) {
+      const int f = q * 64 + lane, row = f / CH, c = f % CH;
+      const int m = mr + row, n = n0 + c * 4;
+      x[q] = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 4);
+      hv[q] = m < M ? *reinterpret_cast<const f32x4*>(hb + (size_t)m * N + n) : f32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int q = 0; q < IT; ++q) {
+      const int f = q * 64 + lane, row = f / CH, c = f % CH;
+      const int m = mr + row, n = n0 + c * 4;
+      if (m < M) {
+        const f32x4 g = *reinterpret_cast<const f32x4*>(ep.gate + (size_t)branch_of(m) * ep.gate_stride + n);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(ep.bias + n);
+        f32x4 y;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[r] = hv[q][r] + g[r] * (x[q][r] + b[r]);
+        *reinterpret_cast<f32x4*>(hb + (size_t)m * N + n) = y;
+      }
+    }
+  }
 
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    // prefetch the next k-tile (the last iteration re-reads the last tile;
-    // it is not stored)
-    const int knext = (kt + 1 < KT ? kt + 1 : kt) * kBK;
+  __device__ __forceinline__ void rows_qkv(const float* strip, int lane, int mr, int n0) const {
+    const int hd = ep.head_dim, hidden = ep.hidden, rpb = ep.rows_per_batch;
+    const size_t ntot = (size_t)ep.kv_tokens;
+    bf16* qb = reinterpret_cast<bf16*>(ep.q);
+    bf16* kvb = reinterpret_cast<bf16*>(ep.kv);
+    // Q and K: 8 channels of one head per lane (head_dim % 8 == 0)
+    if (n0 < 2 * hidden) {
+      constexpr int CH = TN / 8, IT = 32 * CH / 64;
 #pragma unroll
-    for (int i = 0; i < LA; ++i) ra[i] = *reinterpret_cast<const uint4*>(pa[i] + knext);
+      for (int q = 0; q < IT; ++q) {
+        const int f = q * 64 + lane, row = f / CH, c = f % CH;
+        const int m = mr + row, n = n0 + c * 8;
+        if (m >= M || n >= 2 * hidden) continue;
+        const f32x4 x0 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8);
+        const f32x4 x1 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8 + 4);
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(ep.bias + n);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(ep.bias + n + 4);
+        const int b = branch_of(m), tok = m - b * rpb;
+        const int which = n >= hidden, nn = n - which * hidden;
+        const int head = nn / hd, dd = nn - head * hd;
+        bf16* dst = which == 0 ? qb + (((size_t)b * ep.heads + head) * rpb + tok) * hd + dd
+                               : kvb + b * ep.kv_branch_stride + ((size_t)head * ntot + ep.tok_offset + tok) * hd + dd;
+        bf16x8 o;
 #pragma unroll
-    for (int i = 0; i < LB; ++i) rb[i] = *reinterpret_cast<const uint4*>(pb[i] + knext);
+        for (int r = 0; r < 4; ++r) {
+          o[r] = from_f<bf16>(x0[r] + b0[r]);
+          o[4 + r] = from_f<bf16>(x1[r] + b1[r]);
+        }
+        *reinterpret_cast<bf16x8*>(dst) = o;
+      }
+    }
+    // V^T [head][d][token]: 8 consecutive tokens of one channel per lane
+    if (n0 + TN > 2 * hidden) {
+      constexpr int IT = TN * 4 / 64;
+#pragma unroll
+      for (int q = 0; q < IT; ++q) {
+        const int f = q * 64 + lane, col = f % TN, grp = f / TN;
+        const int n = n0 + col;
+        if (n < 2 * hidden) continue;
+        float v[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) v[t] = strip[(grp * 8 + t) * LS + col];
+        const float bias = ep.bias[n];
+        const int nn = n - 2 * hidden, head = nn / hd, dd = nn - head * hd;
+        bf16* vt = kvb + ntot * hidden + ((size_t)head * hd + dd) * ntot + ep.tok_offset;
+        const int m = mr + grp * 8;
+        const int b = m < M ? branch_of(m) : 0, tok = m - b * rpb;
+        bf16* dst = vt + b * ep.kv_branch_stride + tok;
+        if (m + 7 < M && tok + 7 < rpb && ((uintptr_t)dst & 15) == 0) {
+          bf16x8 o;
+#pragma unroll
+          for (int t = 0; t < 8; ++t) o[t] = from_f<bf16>(v[t] + bias);
+          *reinterpret_cast<bf16x8*>(dst) = o;
+        } else {
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {
+            const int mm = m + t;
+            if (mm < M) {
+              const int bb = branch_of(mm);
+              vt[bb * ep.kv_branch_stride + (mm - bb * rpb)] = from_f<bf16>(v[t] + bias);
+            }
+          }
+        }
+      }
+    }
+  }
 
-    const bf16* sa = sa_base + buf * (BM * kLdsStride);
-    const bf16* sb = sb_base + buf * (BN * kLdsStride);
+  // the wave's tile: rows [m0, m0 + 32 FM), columns [n0, n0 + TN)
+  __device__ __forceinline__ void run(const f32x16 (&acc)[FM][FN], float* strip, int lane, int m0,
+                                      int n0) const {
+    const int lr = lane & 31, h = lane >> 5;
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      bf16x8 a[FM], b[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(sa + i * 32 * kLdsStride + kk * 16);
+    for (int i = 0; i < FM; ++i) {
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = *reinterpret_cast<const bf16x8*>(sb + j * 32 * kLdsStride + kk * 16);
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int g = 0; g < 4; ++g)
+          *reinterpret_cast<f32x4*>(strip + lr * LS + j * 32 + 8 * g + 4 * h) =
+              f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+      if constexpr (EPI == kEpiStore || EPI == kEpiGelu) rows_store(strip, lane, m0 + 32 * i, n0);
+      else if constexpr (EPI == kEpiResidual) rows_residual(strip, lane, m0 + 32 * i, n0);
+      else rows_qkv(strip, lane, m0 + 32 * i, n0);
     }
-    if (kt + 1 < KT) {
-      bf16* da = &sA[buf ^ 1][0];
-      bf16* db = &sB[buf ^ 1][0];
-#pragma unroll
-      for (int i = 0; i < LA; ++i) *reinterpret_cast<uint4*>(da + la[i]) = ra[i];
-#pragma unroll
-      for (int i = 0; i < LB; ++i) *reinterpret_cast<uint4*>(db + lb[i]) = rb[i];
-    }
-    __syncthreads();
   }
-
-  // accumulator layout of a 32x32 MFMA block: lane holds column lane%32,
-  // register r holds row 8*(r/4) + 4*(lane/32) + r%4.
-  const Epilogue<bf16, EPI> epi{ep, M, N};
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int n = n0 + wn * TN + j * 32 + (lane & 31);
-    const typename Epilogue<bf16, EPI>::Col col = epi.column(n);
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int m = m0 + wm * TM + i * 32 + 8 * g + 4 * (lane >> 5);
-        float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                      acc[i][j][4 * g + 3]};
-        epi.store4(col, m, n, v);
-      }
-  }
-}
+};
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA GEMM with direct-to-LDS loads (global_load_lds_dwordx4) into an
-// S-stage ring of BK-wide k-tiles.  LDS rows hold BK bf16 without padding and
-// are swizzled for the 64-bank LDS, whose ds_read_b128 serves 16 lanes per
-// cycle: with Q = 256 B / row bytes rows per bank sweep, the 16-byte chunk c
-// of row r is stored at chunk c ^ ((r / Q) mod (BK / 8)), so the 16 rows one
-// read cycle touches land on 16 distinct 4-bank groups.  Each wave-level
-// load writes 1 KB (1024 / (2 BK) rows) of a stage; a manual vmcnt wait plus
-// s_barrier publishes a stage, so up to S-1 k-tiles are in flight while one
-// is consumed.  Operand fragments are double buffered across the 16-deep
-// k-steps so LDS reads overlap the MFMAs.  Tiles are visited in XCD-major,
-// row-grouped order so workgroups sharing an XCD's L2 share operand rows.
-
+// bf16 MFMA GEMM.
+//
+// BM x BN x BK block tile over WM x WN waves; each wave owns a (BM/WM) x
+// (BN/WN) block of v_mfma_f32_32x32x16_bf16 accumulators in fp32.  Operands go
+// global -> LDS with the direct-to-LDS load (16 bytes per lane, 1 KB per wave
+// instruction, no register staging) into a ring of S stages.  LDS rows are
+// 2*BK bytes, unpadded; the 16-byte chunks of row r are XOR-swizzled by
+// (r / Q) % CPR so that a fragment read (16 lanes = 16 rows at one logical
+// chunk) touches 64 distinct banks.  One barrier per k-tile; the loads of
+// tile kt+S-1 are interleaved with the MFMAs of tile kt.
 #define ORCH_LDS __attribute__((address_space(3)))
 #define ORCH_GLB __attribute__((address_space(1)))
 
@@ -283,31 +322,55 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int S, bool SCHED, int EPI>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma_kernel(const bf16* __restrict__ A,
-                                                            const bf16* __restrict__ W, int M,
-                                                            int N, int K, int tiles_m, int tiles_n,
-                                                            EpiParams ep) {
-  constexpr int NW = WM * WN;
+constexpr int cmin(int a, int b) { return a < b ? a : b; }
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+// f(integral_constant<int, I>) for I in [B, E)
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// Compile-time layout of one configuration.
+template <int BM, int BN, int BK, int WM, int WN, int S>
+struct GemmGeo {
+  static constexpr int NW = WM * WN;
+  static constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
+  static constexpr int FM = TM / 32, FN = TN / 32;  // 32x32 blocks per wave
+  static constexpr int CPR = BK / 8;                // 16-byte chunks per row
+  static constexpr int RPL = 1024 / (2 * BK);       // rows per wave-level load
+  static constexpr int Q = 128 / BK;                // rows per 256-byte bank sweep
+  static constexpr int IA = BM / (NW * RPL), IB = BN / (NW * RPL);
+  static constexpr int LPT = IA + IB;               // loads per lane per k-tile
+  static constexpr int STAGE = (BM + BN) * BK * 2;  // bytes per stage
+  static constexpr int KK = BK / 16;                // MFMA k-steps per k-tile
+  // next-tile loads issued per k-step: all in the first with two stages (they
+  // get one tile of compute to land), else spread over the k-steps
+  static constexpr int LPK = S == 2 ? LPT : (LPT + KK - 1) / KK;
   static_assert(NW == 4 || NW == 8, "four or eight waves");
   static_assert(BK == 32 || BK == 64, "k-tile");
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int CPR = BK / 8;                // 16-byte chunks per row
-  constexpr int RPL = 1024 / (2 * BK);       // rows per wave-level load
-  constexpr int Q = 128 / BK;                // rows per 256-byte bank sweep
+  static_assert(FM >= 1 && FN >= 1 && TM % 32 == 0 && TN % 32 == 0, "wave tile");
   static_assert(BM % (NW * RPL) == 0 && BN % (NW * RPL) == 0, "rows per wave");
-  constexpr int IA = BM / (NW * RPL), IB = BN / (NW * RPL);
-  constexpr int LPT = IA + IB;               // loads per thread per stage
-  constexpr int STAGE = (BM + BN) * BK;      // bf16 elements per stage
-  constexpr int KK = BK / 16;
-  static_assert(S >= 2 && LPT * (S - 1) < 64, "pipeline depth");
+  static_assert(S >= 2 && S <= 8 && LPT * (S - 1) < 64, "pipeline depth");
+  static_assert(S * STAGE <= 160 * 1024, "LDS");
+};
 
-  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
+template <int BM, int BN, int BK, int WM, int WN, int S, int EPI>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(const bf16* __restrict__ A,
+                                                        const bf16* __restrict__ W, int M, int N,
+                                                        int K, int tiles_m, int tiles_n,
+                                                        EpiParams ep) {
+  using G = GemmGeo<BM, BN, BK, WM, WN, S>;
+  constexpr int FM = G::FM, FN = G::FN, KK = G::KK, IA = G::IA, LPT = G::LPT, LPK = G::LPK;
+
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
   // tile order: XCD-major, then groups of 8 tile rows, column-major inside
@@ -323,37 +386,22 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma_kernel(const bf16*
   const int tile_n = (pid % (GROUP * tiles_n)) / gsz;
   const int m0 = tile_m * BM, n0 = tile_n * BN;
 
-  // this lane's source chunk of each wave-level load
-  const int prow = lane / CPR;          // row inside the 1 KB block
-  const int pchunk = lane % CPR;        // physical chunk it fills
-  const bf16* srcA[IA];
-  const bf16* srcB[IB];
+  // byte offset of this lane's source chunk in each wave-level load: load j
+  // covers tile rows (j * NW + wave) * RPL .. + RPL - 1 (A rows first, then
+  // W rows); A rows past M re-read row M - 1
+  const int prow = lane / G::CPR;
+  const int pchunk = lane % G::CPR;
+  unsigned off[LPT];
 #pragma unroll
-  for (int i = 0; i < IA; ++i) {
-    const int r = (i * NW + wave) * RPL + prow;
-    const int lchunk = pchunk ^ ((r / Q) % CPR);
-    srcA[i] = A + (size_t)min(m0 + r, M - 1) * K + lchunk * 8;
+  for (int j = 0; j < LPT; ++j) {
+    const int i = j < IA ? j : j - IA;
+    const int r = (i * G::NW + wave) * G::RPL + prow;
+    const int lchunk = pchunk ^ ((r / G::Q) % G::CPR);
+    const unsigned row = j < IA ? (unsigned)min(m0 + r, M - 1) : (unsigned)(n0 + r);
+    off[j] = (row * (unsigned)K + lchunk * 8) * 2u;
   }
-#pragma unroll
-  for (int i = 0; i < IB; ++i) {
-    const int r = (i * NW + wave) * RPL + prow;
-    const int lchunk = pchunk ^ ((r / Q) % CPR);
-    srcB[i] = W + (size_t)(n0 + r) * K + lchunk * 8;
-  }
-
-  auto issue = [&](int kt, int st) {
-    bf16* sa = smem + st * STAGE;
-    bf16* sb = sa + BM * BK;
-    const int ko = kt * BK;
-#pragma unroll
-    for (int i = 0; i < IA; ++i)
-      __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)(srcA[i] + ko),
-                                       (ORCH_LDS void*)(sa + (i * NW + wave) * RPL * BK), 16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < IB; ++i)
-      __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)(srcB[i] + ko),
-                                       (ORCH_LDS void*)(sb + (i * NW + wave) * RPL * BK), 16, 0, 0);
-  };
+  const char* gA = reinterpret_cast<const char*>(A);
+  const char* gW = reinterpret_cast<const char*>(W);
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -363,98 +411,89 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma_kernel(const bf16*
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // operand read offsets: row r = (wave tile row) + lrow; logical chunk 2 kk + h
+  // fragment read offsets: row = wave tile row + lrow, logical chunk 2 kk + h
   const int lrow = lane & 31;
   const int h = lane >> 5;
   int koff[KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) koff[kk] = ((2 * kk + h) ^ ((lrow / Q) % CPR)) * 8;
-  const int arow = (wm * TM + lrow) * BK;
-  const int brow = BM * BK + (wn * TN + lrow) * BK;
+  for (int kk = 0; kk < KK; ++kk) koff[kk] = ((2 * kk + h) ^ ((lrow / G::Q) % G::CPR)) * 16;
+  const int arow = (wm * G::TM + lrow) * BK * 2;
+  const int brow = BM * BK * 2 + (wn * G::TN + lrow) * BK * 2;
 
-  auto compute = [&](int st) {
-    const bf16* base = smem + st * STAGE;
+  const int KT = K / BK;  // >= S - 1 (checked by the launcher)
+
+  // load j of k-tile kt into stage st
+  auto dma = [&](auto jc, int kt_, int st_) {
+    constexpr int j = decltype(jc)::value;
+    constexpr int i = j < IA ? j : j - IA;
+    constexpr int part = j < IA ? 0 : BM * BK * 2;
+    char* dst = smem + st_ * G::STAGE + part + (i * G::NW + wave) * G::RPL * BK * 2;
+    const char* src = (j < IA ? gA : gW) + (unsigned)kt_ * (BK * 2) + off[j];
+    __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src, (ORCH_LDS void*)dst, 16, 0, 0);
+  };
+
+  // the MFMAs of stage st; with issue, the loads of tile ikt into stage ist
+  // go between them.  Emission order is fixed slot by slot (a scheduling
+  // fence after each): MFMA e of k-step kk, then its share of the reads of
+  // k-step kk+1's fragments, then its share of the next tile's loads.
+  auto compute = [&](int st, auto issue_c, int ikt, int ist) {
+    constexpr bool ISSUE = decltype(issue_c)::value;
+    constexpr int NM = FM * FN, ND = FM + FN;
+    const char* base = smem + st * G::STAGE;
     bf16x8 a[2][FM], b[2][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
-      a[0][i] = *reinterpret_cast<const bf16x8*>(base + arow + i * 32 * BK + koff[0]);
+      a[0][i] = *reinterpret_cast<const bf16x8*>(base + arow + i * 32 * BK * 2 + koff[0]);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
-      b[0][j] = *reinterpret_cast<const bf16x8*>(base + brow + j * 32 * BK + koff[0]);
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < KK) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-          a[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(base + arow + i * 32 * BK + koff[kk + 1]);
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          b[cur ^ 1][j] = *reinterpret_cast<const bf16x8*>(base + brow + j * 32 * BK + koff[kk + 1]);
-      }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
-    }
-    if constexpr (SCHED) {
-      // reads of k-step 0, then per k-step: one MFMA, one read of the next
-      // k-step's fragments, ... (masks: 0x8 MFMA, 0x100 DS read)
-      __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        if (kk + 1 < KK) {
-#pragma unroll
-          for (int e = 0; e < FM + FN; ++e) {
-            __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          }
-          if (FM * FN > FM + FN) __builtin_amdgcn_sched_group_barrier(0x8, FM * FN - FM - FN, 0);
-        } else {
-          __builtin_amdgcn_sched_group_barrier(0x8, FM * FN, 0);
-        }
-      }
-    }
+      b[0][j] = *reinterpret_cast<const bf16x8*>(base + brow + j * 32 * BK * 2 + koff[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, KK>([&](auto kkc) {
+      constexpr int kk = decltype(kkc)::value;
+      constexpr int cur = kk & 1;
+      constexpr int nd = kk + 1 < KK ? ND : 0;
+      constexpr int l0 = cmin(kk * LPK, LPT), nl = ISSUE ? cmin(kk * LPK + LPK, LPT) - l0 : 0;
+      static_for<0, NM>([&](auto ec) {
+        constexpr int e = decltype(ec)::value;
+        constexpr int i = e / FN, j = e % FN;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[cur][j], a[cur][i], acc[i][j], 0, 0, 0);
+        static_for<e * nd / NM, (e + 1) * nd / NM>([&](auto dc) {
+          constexpr int d = decltype(dc)::value;
+          if constexpr (d < FM)
+            a[cur ^ 1][d] = *reinterpret_cast<const bf16x8*>(base + arow + d * 32 * BK * 2 + koff[kk + 1]);
+          else
+            b[cur ^ 1][d - FM] =
+                *reinterpret_cast<const bf16x8*>(base + brow + (d - FM) * 32 * BK * 2 + koff[kk + 1]);
+        });
+        static_for<l0 + e * nl / NM, l0 + (e + 1) * nl / NM>([&](auto jc) { dma(jc, ikt, ist); });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
   };
 
-  const int KT = K / BK;  // >= S - 1 (checked by the launcher)
 #pragma unroll
-  for (int s = 0; s < S - 1; ++s) issue(s, s);
+  for (int s = 0; s < S - 1; ++s) static_for<0, LPT>([&](auto jc) { dma(jc, s, s); });
   int kt = 0;
   for (; kt + S - 1 < KT; ++kt) {
     wait_vmcnt<(S - 2) * LPT>();
     lds_barrier();
-    issue(kt + S - 1, (kt + S - 1) % S);
-    compute(kt % S);
+    compute(kt % S, std::true_type{}, kt + S - 1, (kt + S - 1) % S);
   }
   // drain: the last S-1 tiles, nothing more to issue
-  if constexpr (S >= 5) {
-    wait_vmcnt<3 * LPT>(); lds_barrier(); compute(kt % S); ++kt;
-  }
-  if constexpr (S >= 4) {
-    wait_vmcnt<2 * LPT>(); lds_barrier(); compute(kt % S); ++kt;
-  }
-  if constexpr (S >= 3) {
-    wait_vmcnt<LPT>(); lds_barrier(); compute(kt % S); ++kt;
-  }
-  wait_vmcnt<0>(); lds_barrier(); compute(kt % S);
+  static_for<0, S - 2>([&](auto rc) {
+    wait_vmcnt<(S - 2 - decltype(rc)::value) * LPT>();
+    lds_barrier();
+    compute(kt % S, std::false_type{}, 0, 0);
+    ++kt;
+  });
+  wait_vmcnt<0>(); lds_barrier(); compute(kt % S, std::false_type{}, 0, 0);
 
-  const Epilogue<bf16, EPI> epi{ep, M, N};
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int n = n0 + wn * TN + j * 32 + lrow;
-    const typename Epilogue<bf16, EPI>::Col col = epi.column(n);
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int m = m0 + wm * TM + i * 32 + 8 * g + 4 * h;
-        float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                      acc[i][j][4 * g + 3]};
-        epi.store4(col, m, n, v);
-      }
-  }
+  // epilogue: the stage buffers become per-wave staging strips
+  using E = StripEpilogue<FM, FN, EPI>;
+  static_assert(G::NW * E::BYTES <= S * G::STAGE, "epilogue staging fits the stage buffers");
+  lds_barrier();
+  const E epi{ep, M, N};
+  epi.run(acc, reinterpret_cast<float*>(smem + wave * E::BYTES), lane, m0 + wm * G::TM, n0 + wn * G::TN);
 }
 
 // ---------------------------------------------------------------------------
@@ -516,16 +555,17 @@ __global__ __launch_bounds__(256) void gemm_simt_kernel(const T* __restrict__ A,
 // ---------------------------------------------------------------------------
 // Tile selection.  ORCH_GEMM_TILE=<index> forces a configuration (tuning).
 struct TileCfg {
-  int bm, bn, bk, stages;  // stages 0: register-staged kernel
+  int bm, bn, bk, waves, stages;
+  float eff;  // measured relative throughput of the shape on a full machine
 };
 static const TileCfg kTiles[] = {
-    {128, 128, 64, 0}, {256, 128, 64, 0}, {128, 64, 64, 0},      // register staged
-    {128, 128, 64, 3}, {256, 128, 64, 3}, {256, 192, 64, 2},     // LDS DMA, 4 waves
-    {128, 128, 64, 3}, {256, 128, 64, 3}, {256, 192, 64, 2},     //   + sched groups
-    {256, 128, 64, 3}, {256, 192, 64, 2}, {256, 128, 32, 5},     // 8 waves + sched
-    {128, 128, 64, 4}, {256, 64, 64, 4},                         // 8 waves + sched
+    {256, 256, 64, 8, 2, 0.80f},
+    {256, 192, 64, 8, 2, 1.00f},
+    {128, 128, 64, 8, 4, 0.75f},
+    {128, 64, 64, 4, 2, 0.30f},  // fallback: any N % 64 == 0, K % 64 == 0
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
+constexpr int kFallbackTile = kNumTiles - 1;
 
 static int forced_tile() {
   const char* s = getenv("ORCH_GEMM_TILE");
@@ -533,85 +573,79 @@ static int forced_tile() {
 }
 
 static bool tile_fits(const TileCfg& t, int N, int K) {
-  if (N % t.bn || K % t.bk) return false;
-  if (t.stages && K / t.bk < t.stages - 1) return false;
-  return true;
+  return N % t.bn == 0 && K % t.bk == 0 && K / t.bk >= t.stages - 1;
 }
 
-// Pick the configuration with the least estimated time per CU: whole rounds
-// of tiles over the 256 CUs times the tile area, divided by the measured
-// relative efficiency of the tile shape.
+// Pick the configuration with the least estimated time: whole rounds of tiles
+// over the 256 CUs times the tile area, divided by the tile's relative
+// throughput per CU.  The throughputs were measured on the DiT-XL projection
+// shapes (K = 1152 and 4608, M from 768 to 8192): the 256x192 tile is the
+// fastest per CU, the 256x256 one wins when it fills the machine in one round
+// where 256x192 needs two, and the 128x128 one when 256-row tiles would leave
+// most CUs idle.
 static int pick_tile(int M, int N, int K) {
   const int f = forced_tile();
   if (f >= 0 && f < kNumTiles && tile_fits(kTiles[f], N, K)) return f;
-  struct Cand { int idx; float eff; };
-  static const Cand cands[] = {{10, 1.0f}, {9, 0.85f}, {12, 0.75f}};
-  int best = -1;
+  int best = kFallbackTile;
   float best_cost = 0.0f;
-  for (const Cand& c : cands) {
-    const TileCfg& t = kTiles[c.idx];
+  for (int c = 0; c < kNumTiles; ++c) {
+    const TileCfg& t = kTiles[c];
     if (!tile_fits(t, N, K)) continue;
     const int tiles = ceil_div(M, t.bm) * (N / t.bn);
-    const float cost = (float)ceil_div(tiles, 256) * t.bm * t.bn / c.eff;
-    if (best < 0 || cost < best_cost) {
-      best = c.idx;
+    const float cost = (float)ceil_div(tiles, 256) * t.bm * t.bn / t.eff;
+    if (best_cost == 0.0f || cost < best_cost) {
+      best = c;
       best_cost = cost;
     }
   }
-  if (best >= 0) return best;
-  if (N % 128 == 0) return 0;
-  return 2;
+  return best;
 }
 
 bool gemm_uses_mfma(int N, int K, int dtype) {
-  return dtype == kBF16 && N % 64 == 0 && K % kBK == 0;
+  return dtype == kBF16 && N % 64 == 0 && K % 64 == 0;
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
-static void launch_cfg(const void* A, const void* W, int M, int N, int K, const EpiParams& ep,
-                       hipStream_t s) {
-  dim3 grid(N / BN, ceil_div(M, BM));
-  hipLaunchKernelGGL((gemm_bf16_mfma_kernel<BM, BN, WM, WN, EPI>), grid, dim3(64 * WM * WN), 0, s,
-                     reinterpret_cast<const bf16*>(A), reinterpret_cast<const bf16*>(W), M, N, K,
-                     ep);
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// The MFMA kernel moves 16-byte chunks of every operand and output; shapes
+// or pointers that do not allow that take the SIMT kernel.
+static bool mfma_path_ok(const void* A, const void* W, int N, int K, int epi, const EpiParams& ep,
+                         int dtype) {
+  if (!gemm_uses_mfma(N, K, dtype) || !aligned16(A) || !aligned16(W) || !aligned16(ep.bias))
+    return false;
+  if (epi == kEpiResidual) return aligned16(ep.out) && aligned16(ep.gate) && ep.gate_stride % 4 == 0;
+  if (epi == kEpiQkv)
+    return aligned16(ep.q) && aligned16(ep.kv) && ep.head_dim % 8 == 0 && ep.kv_branch_stride % 8 == 0;
+  return aligned16(ep.out);
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int S, bool SCHED, int EPI>
-static void launch_dma(const void* A, const void* W, int M, int N, int K, const EpiParams& ep,
-                       hipStream_t s) {
+template <int BM, int BN, int BK, int WM, int WN, int S, int EPI>
+static void launch_tile(const void* A, const void* W, int M, int N, int K, const EpiParams& ep,
+                        hipStream_t s) {
   const int tm = ceil_div(M, BM), tn = N / BN;
-  const size_t lds = (size_t)S * (BM + BN) * BK * sizeof(bf16);
-  auto kern = gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, S, SCHED, EPI>;
+  constexpr int lds = S * GemmGeo<BM, BN, BK, WM, WN, S>::STAGE;
+  auto kern = gemm_bf16_kernel<BM, BN, BK, WM, WN, S, EPI>;
   static bool attr = [&] {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     return true;
   }();
   (void)attr;
-  hipLaunchKernelGGL(kern, dim3(tm * tn), dim3(64 * WM * WN), lds, s, reinterpret_cast<const bf16*>(A),
-                     reinterpret_cast<const bf16*>(W), M, N, K, tm, tn, ep);
+  hipLaunchKernelGGL(kern, dim3(tm * tn), dim3(64 * WM * WN), lds, s,
+                     reinterpret_cast<const bf16*>(A), reinterpret_cast<const bf16*>(W), M, N, K,
+                     tm, tn, ep);
 }
 
 template <int EPI>
 static hipError_t launch_gemm_epi(const void* A, const void* W, int M, int N, int K,
                                   const EpiParams& ep, int dtype, hipStream_t s) {
   if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
-  if (gemm_uses_mfma(N, K, dtype)) {
+  if (mfma_path_ok(A, W, N, K, EPI, ep, dtype)) {
     switch (pick_tile(M, N, K)) {
-      case 0: launch_cfg<128, 128, 2, 2, EPI>(A, W, M, N, K, ep, s); break;
-      case 1: launch_cfg<256, 128, 2, 2, EPI>(A, W, M, N, K, ep, s); break;
-      case 2: launch_cfg<128, 64, 2, 2, EPI>(A, W, M, N, K, ep, s); break;
-      case 3: launch_dma<128, 128, 64, 2, 2, 3, false, EPI>(A, W, M, N, K, ep, s); break;
-      case 4: launch_dma<256, 128, 64, 2, 2, 3, false, EPI>(A, W, M, N, K, ep, s); break;
-      case 5: launch_dma<256, 192, 64, 2, 2, 2, false, EPI>(A, W, M, N, K, ep, s); break;
-      case 6: launch_dma<128, 128, 64, 2, 2, 3, true, EPI>(A, W, M, N, K, ep, s); break;
-      case 7: launch_dma<256, 128, 64, 2, 2, 3, true, EPI>(A, W, M, N, K, ep, s); break;
-      case 8: launch_dma<256, 192, 64, 2, 2, 2, true, EPI>(A, W, M, N, K, ep, s); break;
-      case 9: launch_dma<256, 128, 64, 4, 2, 3, true, EPI>(A, W, M, N, K, ep, s); break;
-      case 10: launch_dma<256, 192, 64, 4, 2, 2, true, EPI>(A, W, M, N, K, ep, s); break;
-      case 11: launch_dma<256, 128, 32, 4, 2, 5, true, EPI>(A, W, M, N, K, ep, s); break;
-      case 12: launch_dma<128, 128, 64, 4, 2, 4, true, EPI>(A, W, M, N, K, ep, s); break;
-      case 13: launch_dma<256, 64, 64, 4, 2, 4, true, EPI>(A, W, M, N, K, ep, s); break;
+      case 0: launch_tile<256, 256, 64, 2, 4, 2, EPI>(A, W, M, N, K, ep, s); break;
+      case 1: launch_tile<256, 192, 64, 4, 2, 2, EPI>(A, W, M, N, K, ep, s); break;
+      case 2: launch_tile<128, 128, 64, 4, 2, 4, EPI>(A, W, M, N, K, ep, s); break;
+      default: launch_tile<128, 64, 64, 2, 2, 2, EPI>(A, W, M, N, K, ep, s); break;
     }
   } else {
     dim3 grid(ceil_div(N, simt_gemm::BN), ceil_div(M, simt_gemm::BM));
