@@ -20,10 +20,9 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liborch.so")
 SOURCES = ["k_gemm.hip", "k_attention.hip", "k_misc.hip", "orch_abi.hip"]
-# per-source extra flags: attention keeps MFMA accumulators in VGPRs (its
-# softmax works on the scores with VALU ops, which would otherwise copy them
-# out of AGPRs every tile)
-EXTRA = {"k_attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+# per-source extra flags: attention is built without IEEE NaN quieting, so the
+# row max of the online softmax is plain v_max3_f32
+EXTRA = {"k_attention.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans"]}
 ARCH = "gfx950"
 
 

@@ -7,17 +7,18 @@
 // Scores are formed transposed, S^T = K Q^T, so that a lane owns one query
 // column: the running max of the online softmax stays in-lane, and the
 // probabilities it holds are directly the B operand of O^T = V^T P^T.
-// K tiles ([64 keys][d]) and V^T tiles ([d][64 keys]) are staged through
-// double-buffered LDS; the V^T layout of the buffer makes both tile loads
-// contiguous 16-byte rows.  In LDS the keys of each 16-key chunk of V^T are
-// permuted so that the 8 keys a lane's P fragment covers are contiguous (one
-// ds_read_b128), and row strides are chosen for the 64-bank LDS.  When the
-// head dimension is padded (d = 72 -> 96 rows of O^T), one padding row of
-// V^T holds ones, so the PV product also accumulates the softmax
-// denominator.  exp2 runs on v_exp_f32 with log2(e)/sqrt(d) folded into the
-// exponent; the running max is raised lazily (only past a 2^8 margin), so
-// O is rarely rescaled.  Built with MFMA accumulators in VGPRs, so the
-// softmax reads the scores without AGPR copies.
+// K tiles ([64 keys][d], rows unpadded) and V^T tiles ([d][64 keys], 16-byte
+// chunks XOR-swizzled by row) go global -> LDS with the direct-to-LDS load
+// into a ring of three stages, one barrier per tile.  K rows are permuted in
+// LDS (bits 2 and 3 of the row swapped) so that the 8 keys of each lane's P
+// fragment are contiguous in natural key order.  When the head dimension is
+// padded (d = 72 -> 96 rows of O^T), one padding row of V^T holds ones, so
+// the PV product also accumulates the softmax denominator.  exp2 runs on
+// v_exp_f32 with log2(e)/sqrt(d) folded into the exponent; the running max is
+// raised lazily (only past a 2^8 margin), so O is rarely rescaled.  The loop
+// runs over 32-key halves of a tile: the MFMAs of the next half's scores are
+// issued between the current half's exponentials, then its PV MFMAs.  Built
+// without IEEE NaN quieting, so the row max is plain v_max3_f32.
 //
 // fp32 path (and unsupported shapes): one thread per query, online softmax.
 #include "common.h"
@@ -26,143 +27,96 @@
 namespace orch {
 
 namespace mfma_attn {
-constexpr int BQ = 128, BKV = 64;
+constexpr int BQ = 128, BKV = 64, NSTAGE = 4;
 
 template <int D>
 struct Geo {
-  static constexpr int DP = (D + 15) / 16 * 16;  // QK^T contraction, padded to 16
-  static constexpr int NC = DP / 16;
-  static constexpr int DV = (D + 31) / 32 * 32;  // rows of O^T, padded to 32
+  static constexpr int NC = (D + 15) / 16;          // 16-dim chunks of S^T = K Q^T
+  static constexpr int NS = 2 * NC;                 // MFMAs of one S^T tile
+  static constexpr int DV = (D + 31) / 32 * 32;     // rows of O^T, padded to 32
   static constexpr int NT = DV / 32;
-  static constexpr bool ONES = DV > D;           // padding row D of V^T holds 1.0
-  // LDS strides in bf16: 16 consecutive rows of a 16-byte column hit 16
-  // distinct 4-bank groups (row stride = 4 * odd banks)
-  static constexpr int KS = ((DP / 2) % 8 == 4) ? DP : DP + 8;
-  static constexpr int VS = BKV + 8;
-  static constexpr int K_CHUNKS = BKV * (D / 8);
-  static constexpr int V_CHUNKS = D * (BKV / 8);
-  static constexpr int K_IT = (K_CHUNKS + 255) / 256;
-  static constexpr int V_IT = (V_CHUNKS + 255) / 256;
-  static constexpr int K_BUF = BKV * KS, V_BUF = DV * VS;
+  static constexpr bool ONES = DV > D;              // padding row D of V^T holds 1.0
+  static constexpr int KROW = 2 * D;                // bytes per K row in LDS
+  static constexpr int KCH = KROW / 16;             // 16-byte chunks per K row
+  static constexpr bool KSWZ = KCH == 8;            // 128-byte rows: XOR swizzle
+  static constexpr int K_BYTES = BKV * KROW;
+  static constexpr int K_SPAN = (K_BYTES + 16 + 255) / 256 * 256;  // 16 zero bytes after K
+  static constexpr int VROW = 2 * BKV;              // bytes per V^T row
+  static constexpr int V_BYTES = D * VROW;
+  static constexpr int STAGE = K_SPAN + V_BYTES;
+  static constexpr int CONST_OFF = NSTAGE * STAGE;  // V^T rows [D, DV), shared by the stages
+  static constexpr int DUMMY_OFF = CONST_OFF + (DV - D) * VROW;  // sink of padding loads
+  static constexpr int LDS = DUMMY_OFF + 1024;
+  static constexpr int K_LOADS = K_BYTES / 1024;    // 1 KB wave-level loads
+  static constexpr int V_LOADS = V_BYTES / 1024;
+  // waves 0-1 load K, waves 2-3 V^T, LPW loads each per tile; slots past the
+  // tile's loads re-read a valid chunk into the sink, so every wave counts
+  // the same number of loads
+  static constexpr int LPW = (cmax(K_LOADS, V_LOADS) + 1) / 2;
+  static_assert(K_BYTES % 1024 == 0 && V_BYTES % 1024 == 0, "whole 1 KB loads");
+  // 16 consecutive K rows at one 16-byte column must hit distinct 4-bank
+  // groups: an odd number of chunks per row, or 8 chunks with the swizzle
+  static_assert(KCH == 8 || KCH % 2 == 1, "K row layout");
+  static_assert(2 * LDS <= 160 * 1024, "two workgroups per CU");
+  static_assert(2 * LPW < 16, "loads in flight");
 };
 
-// Register staging of one K tile ([64 keys][D]) and one V^T tile ([D][64
-// keys]) for 256 threads.  K chunk c: key row c / (D/8), 8-dim chunk c % (D/8).
-// V^T chunk c: dim row c / 8, 8-key chunk kc = c % 8; in LDS the 4+4 keys of
-// that chunk go to positions (kc/2)*16 + (kc%2)*4 and +8, so that within a
-// 16-key group a lane with half h finds keys {4h..4h+3, 8+4h..8+4h+3}
-// contiguous.  Idle slots (the tile does not split evenly over 256 threads)
-// re-read a valid chunk and skip the store.
-template <int D>
-struct Stage {
-  using G = Geo<D>;
-  int k_row[G::K_IT], k_col[G::K_IT], k_dst[G::K_IT], v_row[G::V_IT], v_kc[G::V_IT],
-      v_dst[G::V_IT], k_on[G::K_IT], v_on[G::V_IT];
-  uint4 rk[G::K_IT], rv[G::V_IT];
-
-  __device__ __forceinline__ void init(int tid) {
-#pragma unroll
-    for (int i = 0; i < G::K_IT; ++i) {
-      const int c = tid + 256 * i;
-      k_on[i] = c < G::K_CHUNKS;
-      k_row[i] = k_on[i] ? c / (D / 8) : 0;
-      k_col[i] = k_on[i] ? (c % (D / 8)) * 8 : 0;
-      k_dst[i] = k_row[i] * G::KS + k_col[i];
-    }
-#pragma unroll
-    for (int i = 0; i < G::V_IT; ++i) {
-      const int c = tid + 256 * i;
-      v_on[i] = c < G::V_CHUNKS;
-      v_row[i] = v_on[i] ? c >> 3 : 0;
-      v_kc[i] = v_on[i] ? c & 7 : 0;
-      v_dst[i] = v_row[i] * G::VS + (v_kc[i] >> 1) * 16 + (v_kc[i] & 1) * 4;
-    }
-  }
-  __device__ __forceinline__ void load_k(int n0, const AttnParams& p, const bf16* kf,
-                                         const bf16* ks) {
-#pragma unroll
-    for (int i = 0; i < G::K_IT; ++i) {
-      const int n = n0 + k_row[i];
-      const int f = n - p.fresh_begin;
-      const bf16* src = ((unsigned)f < (unsigned)p.n_fresh) ? kf + (size_t)f * D : ks + (size_t)n * D;
-      rk[i] = *reinterpret_cast<const uint4*>(src + k_col[i]);
-    }
-  }
-  __device__ __forceinline__ void load_v(int n0, const AttnParams& p, const bf16* vf,
-                                         const bf16* vs) {
-#pragma unroll
-    for (int i = 0; i < G::V_IT; ++i) {
-      const int n = n0 + v_kc[i] * 8;
-      const int f = n - p.fresh_begin;
-      const bf16* src = ((unsigned)f < (unsigned)p.n_fresh)
-                            ? vf + (size_t)v_row[i] * p.n_fresh + f
-                            : vs + (size_t)v_row[i] * p.n_kv + n;
-      rv[i] = *reinterpret_cast<const uint4*>(src);
-    }
-  }
-  __device__ __forceinline__ void store_k(bf16* sk) const {
-#pragma unroll
-    for (int i = 0; i < G::K_IT; ++i)
-      if (k_on[i]) *reinterpret_cast<uint4*>(sk + k_dst[i]) = rk[i];
-  }
-  __device__ __forceinline__ void store_v(bf16* sv) const {
-#pragma unroll
-    for (int i = 0; i < G::V_IT; ++i)
-      if (v_on[i]) {
-        *reinterpret_cast<uint2*>(sv + v_dst[i]) = make_uint2(rv[i].x, rv[i].y);
-        *reinterpret_cast<uint2*>(sv + v_dst[i] + 8) = make_uint2(rv[i].z, rv[i].w);
-      }
-  }
-};
-
-// S^T of one 64-key tile: keys [32 sub, +32) x a wave's 32 queries.  `sk`
-// points at this lane's row / half of the K tile in LDS.
-struct Scores {
-  f32x16 v[2];
-};
-
-template <int D>
-__device__ __forceinline__ Scores qk_scores(const bf16* sk, const bf16x8 (&qf)[Geo<D>::NC]) {
-  Scores sc;
-#pragma unroll
-  for (int sub = 0; sub < 2; ++sub) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) sc.v[sub][r] = 0.0f;
-#pragma unroll
-    for (int c = 0; c < Geo<D>::NC; ++c) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(sk + sub * 32 * Geo<D>::KS + c * 16);
-      sc.v[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[c], sc.v[sub], 0, 0, 0);
-    }
-  }
-  return sc;
+// LDS row rho of a K tile holds key kperm(rho): bits 2 and 3 swapped.  The
+// S^T accumulator row 8g + 4h + r then belongs to key 16c + 8h + e for the
+// P fragment (chunk c, element e) a lane with half h feeds to the PV MFMA,
+// i.e. the 8 keys of a lane's fragment are contiguous and V^T stays in
+// natural key order.
+__device__ __forceinline__ int kperm(int rho) {
+  return (rho & ~12) | ((rho & 4) << 1) | ((rho & 8) >> 1);
 }
 
+// word 3 of a raw buffer resource (gfx9: 32-bit data format, no swizzle)
+constexpr int kBufWord3 = 0x00020000;
+
+// Resource of a wave-uniform buffer; the base and size go through
+// readfirstlane so the compiler keeps the descriptor in SGPRs.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, size_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void* ub = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, __builtin_amdgcn_readfirstlane((int)bytes),
+                                           kBufWord3);
+}
 }  // namespace mfma_attn
 
 template <int D>
-__global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
+__global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
+  // the body uses device-only types (buffer resources); the host pass only
+  // needs the launch stub
+#if defined(__HIP_DEVICE_COMPILE__)
   using namespace mfma_attn;
   using G = Geo<D>;
-  constexpr int NC = G::NC, NT = G::NT, DV = G::DV, KS = G::KS, VS = G::VS;
-  constexpr int K_IT = G::K_IT, V_IT = G::V_IT;
-  static_assert(((KS / 2) % 4 == 0) && (((KS / 2) / 4) % 2 == 1), "K stride");
+  constexpr int NC = G::NC, NS = G::NS, NT = G::NT, LPW = G::LPW;
 
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][G::K_BUF];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][G::V_BUF];
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5;
   const int lc = lane & 31;
-  const int b = blockIdx.z;
-  const int head = blockIdx.y;
+  // Workgroups go round-robin over the 8 XCDs; the ones of XCD x take the
+  // x-th contiguous eighth of the (branch, head, split, query tile) order, so
+  // the query tiles that read the same K/V share one L2.
   const int n_qt = (p.n_q + BQ - 1) / BQ;
-  const int split = blockIdx.x / n_qt;            // key split of this workgroup
-  const int q0 = (blockIdx.x - split * n_qt) * BQ;
+  const int T = gridDim.x;
+  int lb = blockIdx.x;
+  if (lb < T / 8 * 8) lb = (lb & 7) * (T / 8) + (lb >> 3);
+  const int qt = lb % n_qt;
+  const int split = (lb / n_qt) % p.splits;       // key split of this workgroup
+  const int pair = lb / (n_qt * p.splits);
+  const int head = pair % p.heads, b = pair / p.heads;
+  const int q0 = qt * BQ;
   const int H = p.heads * D;
   const int kv_len = p.n_kv / p.splits;           // multiple of BKV (launcher)
   const int kv0 = split * kv_len;
+  const int fb = p.fresh_begin, nf = p.n_fresh;
 
   const bf16* qbase = reinterpret_cast<const bf16*>(p.q) + ((size_t)b * p.heads + head) * p.n_q * D;
   const bf16* ks = reinterpret_cast<const bf16*>(p.kv_stale) + b * p.stale_bs +
@@ -171,26 +125,16 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
                    (size_t)p.n_kv * H + (size_t)head * D * p.n_kv;
   const bf16* kf = ks;
   const bf16* vf = vs;
-  if (p.n_fresh > 0) {
-    kf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)head * p.n_fresh * D;
-    vf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)p.n_fresh * H +
-         (size_t)head * D * p.n_fresh;
+  if (nf > 0) {
+    kf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)head * nf * D;
+    vf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)nf * H +
+         (size_t)head * D * nf;
   }
-
-  // padding: K columns [D, KS) are zero; V^T rows [D, DV) are zero except
-  // row D, which is one when present (never overwritten by tile loads)
-  for (int i = tid; i < 2 * BKV * (KS - D); i += 256) {
-    const int buf = i / (BKV * (KS - D));
-    const int rem = i - buf * BKV * (KS - D);
-    sK[buf][(rem / (KS - D)) * KS + D + rem % (KS - D)] = (bf16)0.0f;
-  }
-  if constexpr (DV > D) {
-    for (int i = tid; i < 2 * (DV - D) * VS; i += 256) {
-      const int buf = i / ((DV - D) * VS);
-      const int rem = i - buf * (DV - D) * VS;
-      sV[buf][D * VS + rem] = (bf16)(rem < VS ? 1.0f : 0.0f);
-    }
-  }
+  // buffer resources of this (branch, head): out-of-range reads return zero
+  const __amdgpu_buffer_rsrc_t rks = buffer_rsrc(ks, (size_t)p.n_kv * D * 2);
+  const __amdgpu_buffer_rsrc_t rvs = buffer_rsrc(vs, (size_t)p.n_kv * D * 2);
+  const __amdgpu_buffer_rsrc_t rkf = buffer_rsrc(kf, (size_t)(nf > 0 ? nf : p.n_kv) * D * 2);
+  const __amdgpu_buffer_rsrc_t rvf = buffer_rsrc(vf, (size_t)(nf > 0 ? nf : p.n_kv) * D * 2);
 
   // this lane's query (B operand of S^T = K Q^T): Q[q][c*16 + 8h .. +8]
   const int qrow = min(q0 + wave * 32 + lc, p.n_q - 1);
@@ -206,8 +150,107 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
     }
   }
 
-  Stage<D> stg;
-  stg.init(tid);
+  // constant LDS (never written by the tile loads): 16 zero bytes after the
+  // K rows of every stage, read against zero Q padding by the last chunk of
+  // row 63; V^T rows [D, DV): row D ones, the rest zero
+  for (int st = tid; st < NSTAGE * 4; st += 256)
+    reinterpret_cast<uint32_t*>(smem + (st >> 2) * G::STAGE + G::K_BYTES)[st & 3] = 0u;
+  {
+    bf16* cpad = reinterpret_cast<bf16*>(smem + G::CONST_OFF);
+    for (int i = tid; i < (G::DV - D) * BKV; i += 256) cpad[i] = (bf16)(i < BKV ? 1.0f : 0.0f);
+  }
+
+  // This wave's share of a tile's loads.  Waves 0-1 load K: load j = wave +
+  // 2 i fills stage bytes [1024 j, +1024), lane slot s = 64 j + lane is row
+  // s / KCH, physical chunk s % KCH.  Waves 2-3 load V^T: load j = wave - 2 +
+  // 2 i fills K_SPAN + 1024 j, row s / 8, physical chunk s % 8, logical 8-key
+  // chunk = physical ^ ((row >> 1) & 7).  off: byte offset of the lane's
+  // source from the tile's first key in the stale buffer (the same for fresh
+  // K; fresh V^T rows have stride n_fresh).
+  const bool kwave = wave < 2;
+  const int wl = wave & 1;
+  const int nload = kwave ? G::K_LOADS : G::V_LOADS;
+  unsigned off[LPW];
+#pragma unroll
+  for (int i = 0; i < LPW; ++i) {
+    const int j = min(wl + 2 * i, nload - 1);
+    const int sl = j * 64 + lane;
+    if (kwave) {
+      const int rho = sl / G::KCH, pc = sl % G::KCH;
+      const int lch = G::KSWZ ? pc ^ ((rho >> 1) & 7) : pc;
+      off[i] = (unsigned)(kperm(rho) * D + lch * 8) * 2u;
+    } else {
+      const int d = sl >> 3, lch = (sl & 7) ^ ((d >> 1) & 7);
+      off[i] = (unsigned)(d * p.n_kv + lch * 8) * 2u;
+    }
+  }
+  // V^T row of load slot i (V waves)
+  auto vrow = [&](int i) { return (min(wl + 2 * i, nload - 1) * 64 + lane) >> 3; };
+  auto dst_of = [&](int st, int i) -> ORCH_LDS void* {
+    const int j = wl + 2 * i;
+    if (j >= nload) return (ORCH_LDS void*)(smem + G::DUMMY_OFF);
+    return (ORCH_LDS void*)(smem + st * G::STAGE + (kwave ? 0 : G::K_SPAN) + j * 1024);
+  };
+  auto issue = [&](int n0, int st) {
+    const bool all_stale = n0 + BKV <= fb || n0 >= fb + nf;
+    const bool all_fresh = n0 >= fb && n0 + BKV <= fb + nf;
+    if (all_stale) {
+      const __amdgpu_buffer_rsrc_t r = kwave ? rks : rvs;
+      const unsigned so = __builtin_amdgcn_readfirstlane((unsigned)n0 * (kwave ? 2 * D : 2));
+#pragma unroll
+      for (int i = 0; i < LPW; ++i) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst_of(st, i), 16, off[i], so, 0, 0);
+    } else if (all_fresh) {
+      const __amdgpu_buffer_rsrc_t r = kwave ? rkf : rvf;
+      const unsigned so = __builtin_amdgcn_readfirstlane((unsigned)(n0 - fb) * (kwave ? 2 * D : 2));
+#pragma unroll
+      for (int i = 0; i < LPW; ++i) {
+        const unsigned o = kwave ? off[i] : off[i] - (unsigned)(vrow(i) * (p.n_kv - nf)) * 2u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst_of(st, i), 16, o, so, 0, 0);
+      }
+    } else {
+      // a tile across the band edge: per-lane source (8-key groups are all
+      // fresh or all stale: fb, nf % 8 == 0); 32-bit offsets from the
+      // uniform bases keep the loop-invariant part small
+#pragma unroll
+      for (int i = 0; i < LPW; ++i) {
+        const char* base;
+        unsigned bo;
+        if (kwave) {
+          const int e = off[i] / 2, key = e / D, col = e - key * D;
+          const int n = n0 + key;
+          const bool fr = (unsigned)(n - fb) < (unsigned)nf;
+          base = reinterpret_cast<const char*>(fr ? kf : ks);
+          bo = (unsigned)((fr ? n - fb : n) * D + col) * 2u;
+        } else {
+          const int d = vrow(i), key = off[i] / 2 - d * p.n_kv;
+          const int n = n0 + key;
+          const bool fr = (unsigned)(n - fb) < (unsigned)nf;
+          base = reinterpret_cast<const char*>(fr ? vf : vs);
+          bo = (unsigned)(fr ? d * nf + (n - fb) : d * p.n_kv + n) * 2u;
+        }
+        __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)(base + bo), dst_of(st, i), 16, 0, 0);
+      }
+    }
+  };
+  // wait until at most `tiles` tiles of this wave's loads are in flight
+  auto wait_tiles = [&](int tiles) {
+    if (tiles <= 0) wait_vmcnt<0>();
+    else if (tiles == 1) wait_vmcnt<LPW>();
+    else wait_vmcnt<2 * LPW>();
+  };
+
+  // fragment read offsets: K row sub*32 + lc, logical chunk 2c + h; V^T row
+  // t*32 + lc, logical chunk 2c + h (the swizzle depends on lc only).  V^T
+  // rows >= D are the shared constant rows.
+  int k_rd[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+    k_rd[c] = lc * G::KROW + (G::KSWZ ? ((2 * c + h) ^ ((lc >> 1) & 7)) : (2 * c + h)) * 16;
+  int v_rd[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v_rd[c] = lc * G::VROW + ((2 * c + h) ^ ((lc >> 1) & 7)) * 16;
+  const bool last_in_pad = (NT - 1) * 32 + lc >= D;   // row of the last O^T tile is padding
+
   const float scale = 1.4426950408889634f / sqrtf((float)D);  // log2(e) / sqrt(d)
   float m_run = -1e30f, l_run = 0.0f;
   f32x16 o[NT];
@@ -216,34 +259,35 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
 
-  const int k_rd = lc * KS + h * 8;   // + sub*32*KS + c*16
-  const int v_rd = lc * VS + h * 8;   // + t*32*VS + c*16
-
-  // Key tiles: K and V^T of tile it in sK / sV[it & 1]; the next tile is
-  // loaded into registers during this one and stored before the barrier.
-  // The loads are unconditional (past the end they re-read the last tile,
-  // which is then not stored) so the staging stays in registers.
-  const int NIT = kv_len / BKV;
-  stg.load_k(kv0, p, kf, ks);
-  stg.load_v(kv0, p, vf, vs);
-  stg.store_k(sK[0]);
-  stg.store_v(sV[0]);
-  __syncthreads();
-
-  for (int it = 0; it < NIT; ++it) {
-    const int buf = it & 1;
-    stg.load_k(kv0 + min(it + 1, NIT - 1) * BKV, p, kf, ks);
-    stg.load_v(kv0 + min(it + 1, NIT - 1) * BKV, p, vf, vs);
-    const Scores sc = qk_scores<D>(sK[buf] + k_rd, qf);
-
-    // online softmax over this lane's query column.  The running max is only
-    // raised when some lane's tile max exceeds it by more than 8 (log2
-    // units): until then exp2(s - m_run) <= 2^8, exact in fp32 and in range
-    // for bf16, and O and the denominator keep a common scale, so O is
-    // rarely rescaled.
-    float mx = fmaxf(sc.v[0][0], sc.v[1][0]);
+  // K fragments of half `sub` (keys [32 sub, +32)) of the tile in stage st
+  auto k_frags = [&](int st, int sub, bf16x8(&kf_)[NC]) {
+    const char* sk = smem + st * G::STAGE + sub * 32 * G::KROW;
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sc.v[0][r], sc.v[1][r]));
+    for (int c = 0; c < NC; ++c) kf_[c] = *reinterpret_cast<const bf16x8*>(sk + k_rd[c]);
+  };
+  // V^T fragment of O^T tile tt and 16-key chunk c of the tile in stage st
+  auto v_frag = [&](int st, int tt, int c) {
+    const char* src = (tt == NT - 1 && last_in_pad)
+                          ? smem + G::CONST_OFF + (tt * 32 + lc - D) * G::VROW + (v_rd[c] - lc * G::VROW)
+                          : smem + st * G::STAGE + G::K_SPAN + tt * 32 * G::VROW + v_rd[c];
+    return *reinterpret_cast<const bf16x8*>(src);
+  };
+
+  // One 32-key half of a tile: scores sc = S^T of keys [32 sub, +32) of the
+  // tile in stage st.  With NEXT, the MFMAs of the next half's scores (K
+  // fragments kn, result sn) are issued between the exponentials; then
+  // O^T += V^T P^T over the half's two 16-key chunks.
+  auto half = [&](auto next_c, int st, int sub, const f32x16& sc, const bf16x8(&kn)[NC],
+                  f32x16& sn) {
+    constexpr bool NEXT = decltype(next_c)::value;
+    // online softmax over this lane's query column.  The running max is only
+    // raised when some lane's max exceeds it by more than 8 (log2 units):
+    // until then exp2(s - m_run) <= 2^8, exact in fp32 and in range for
+    // bf16, and O and the denominator keep a common scale, so O is rarely
+    // rescaled.
+    float mx = fmaxf(sc[0], sc[1]);
+#pragma unroll
+    for (int r = 2; r < 16; r += 2) mx = fmaxf(mx, fmaxf(sc[r], sc[r + 1]));
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale;
     float alpha = 1.0f;
     if (__any(mx > m_run + 8.0f)) {
@@ -251,41 +295,73 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
       alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+      for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+        for (int r = 0; r < 16; ++r) o[tt][r] *= alpha;
+    }
+    if constexpr (NEXT) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sn[r] = 0.0f;
     }
     float psum = 0.0f;
-    bf16x8 pf[4];
+    bf16x8 pf[2];
+    static_for<0, 2>([&](auto cc) {
+      constexpr int ci = decltype(cc)::value;
+      if constexpr (NEXT) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int sub = c >> 1;
-      const int g0 = 2 * (c & 1);
+        for (int c = ci * NC / 2; c < (ci + 1) * NC / 2; ++c)
+          sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], sn, 0, 0, 0);
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int r = 4 * (g0 + (e >> 2)) + (e & 3);
-        const float pv = __builtin_amdgcn_exp2f(fmaf(sc.v[sub][r], scale, -m_run));
+        const int r = 4 * (2 * ci + (e >> 2)) + (e & 3);
+        const float pv = __builtin_amdgcn_exp2f(fmaf(sc[r], scale, -m_run));
         if constexpr (!G::ONES) psum += pv;
-        pf[c][e] = (bf16)pv;
+        pf[ci][e] = (bf16)pv;
       }
-    }
+    });
     if constexpr (!G::ONES) l_run = l_run * alpha + psum;
+    // chunk-major, so consecutive MFMAs accumulate into different O^T tiles
+#pragma unroll
+    for (int ci = 0; ci < 2; ++ci)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt)
+        o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(st, tt, 2 * sub + ci), pf[ci], o[tt], 0, 0, 0);
+  };
 
-    // O^T += V^T P^T
-    const bf16* sv = sV[buf];
+  const int NIT = kv_len / BKV;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < NIT) issue(kv0 + s * BKV, s);
+  wait_tiles(min(NIT - 1, NSTAGE - 2));
+  lds_barrier();
+
+  // scores ping-pong between s0 (first halves) and s1 (second halves)
+  f32x16 s0, s1;
+  bf16x8 kn[NC];
+  k_frags(0, 0, kn);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(sv + v_rd + t * 32 * VS + c * 16);
-        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[c], o[t], 0, 0, 0);
-      }
-    }
-    if (it + 1 < NIT) {
-      stg.store_k(sK[buf ^ 1]);
-      stg.store_v(sV[buf ^ 1]);
-    }
-    __syncthreads();
+  for (int r = 0; r < 16; ++r) s0[r] = 0.0f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], s0, 0, 0, 0);
+
+  int t = 0;
+  for (; t + 1 < NIT; ++t) {
+    const int st = t % NSTAGE;
+    k_frags(st, 1, kn);
+    half(std::true_type{}, st, 0, s0, kn, s1);
+    // tile t+1 resident; stage (t-1) % NSTAGE is free for tile t+3
+    wait_tiles(t + 2 < NIT ? 1 : 0);
+    lds_barrier();
+    if (t + NSTAGE - 1 < NIT) issue(kv0 + (t + NSTAGE - 1) * BKV, (t + NSTAGE - 1) % NSTAGE);
+    k_frags((t + 1) % NSTAGE, 0, kn);
+    half(std::true_type{}, st, 1, s1, kn, s0);
+  }
+  {
+    const int st = t % NSTAGE;
+    k_frags(st, 1, kn);
+    half(std::true_type{}, st, 0, s0, kn, s1);
+    half(std::false_type{}, st, 1, s1, kn, s0);
   }
 
   // softmax denominator: the ones row D of O^T (register 4*((D%32)/8) + D%4
@@ -333,6 +409,7 @@ __global__ __launch_bounds__(256) void attn_bf16_mfma_kernel(AttnParams p) {
         }
       }
   }
+#endif
 }
 
 // Combine of the key splits: O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s
@@ -450,11 +527,30 @@ size_t attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int d, int
   return part_o_bytes(s, B, n_q, heads * d) + (size_t)s * B * heads * n_q * sizeof(float2);
 }
 
+static bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15) == 0; }
+
+template <int D>
+static void launch_mfma(dim3 grid, const AttnParams& p, hipStream_t s) {
+  constexpr int lds = mfma_attn::Geo<D>::LDS;
+  auto kern = attn_bf16_mfma_kernel<D>;
+  static bool attr = [&] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    return true;
+  }();
+  (void)attr;
+  hipLaunchKernelGGL(kern, grid, dim3(256), lds, s, p);
+}
+
 hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
   if (p0.n_q <= 0) return hipSuccess;
   AttnParams p = p0;
   p.splits = 1;
-  const bool aligned = (p.fresh_begin % 8 == 0) && (p.n_fresh % 8 == 0);
+  // the MFMA kernel moves 16-byte chunks of Q, K and V^T (8 keys of V^T at a
+  // time, all fresh or all stale)
+  const bool aligned = p.fresh_begin % 8 == 0 && p.n_fresh % 8 == 0 && aligned16(p.q) &&
+                       aligned16(p.kv_stale) && p.stale_bs % 8 == 0 &&
+                       (p.n_fresh == 0 || (aligned16(p.kv_fresh) && p.fresh_bs % 8 == 0));
   if (attention_uses_mfma(p.d, p.n_kv, dtype) && aligned) {
     const int want = pick_splits(p.B, p.heads, p.n_q, p.n_kv);
     if (want > 1 && p.ws &&
@@ -464,11 +560,11 @@ hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
       p.part_ml = reinterpret_cast<float2*>(reinterpret_cast<char*>(p.ws) +
                                             part_o_bytes(want, p.B, p.n_q, p.heads * p.d));
     }
-    dim3 grid(ceil_div(p.n_q, mfma_attn::BQ) * p.splits, p.heads, p.B);
+    dim3 grid(ceil_div(p.n_q, mfma_attn::BQ) * p.splits * p.heads * p.B);
     if (p.d == 64)
-      hipLaunchKernelGGL(attn_bf16_mfma_kernel<64>, grid, dim3(256), 0, s, p);
+      launch_mfma<64>(grid, p, s);
     else
-      hipLaunchKernelGGL(attn_bf16_mfma_kernel<72>, grid, dim3(256), 0, s, p);
+      launch_mfma<72>(grid, p, s);
     if (p.splits > 1) {
       const size_t H = (size_t)p.heads * p.d;
       dim3 g2(ceil_div((int)H, 256), p.B * p.n_q);

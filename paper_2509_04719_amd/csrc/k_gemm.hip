@@ -306,34 +306,6 @@ struct StripEpilogue {
 // (r / Q) % CPR so that a fragment read (16 lanes = 16 rows at one logical
 // chunk) touches 64 distinct banks.  One barrier per k-tile; the loads of
 // tile kt+S-1 are interleaved with the MFMAs of tile kt.
-#define ORCH_LDS __attribute__((address_space(3)))
-#define ORCH_GLB __attribute__((address_space(1)))
-
-// s_waitcnt with vmcnt = n and the other counters left free (gfx9 encoding).
-template <int n>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(n >= 0 && n < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
-}
-
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-constexpr int cmin(int a, int b) { return a < b ? a : b; }
-constexpr int cmax(int a, int b) { return a > b ? a : b; }
-
-// f(integral_constant<int, I>) for I in [B, E)
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (B < E) {
-    f(std::integral_constant<int, B>{});
-    static_for<B + 1, E>(f);
-  }
-}
-
 // Compile-time layout of one configuration.
 template <int BM, int BN, int BK, int WM, int WN, int S>
 struct GemmGeo {
