@@ -228,7 +228,7 @@ struct StripEpilogue {
         const f32x4 b1 = *reinterpret_cast<const f32x4*>(ep.bias + n + 4);
         const int b = branch_of(m), tok = m - b * rpb;
         const int which = n >= hidden, nn = n - which * hidden;
-        const int head = nn / hd, dd = nn - head * hd;
+        const int head = (int)__umulhi((unsigned)nn, ep.hd_magic), dd = nn - head * hd;
         bf16* dst = which == 0 ? qb + (((size_t)b * ep.heads + head) * rpb + tok) * hd + dd
                                : kvb + b * ep.kv_branch_stride + ((size_t)head * ntot + ep.tok_offset + tok) * hd + dd;
         bf16x8 o;
@@ -240,19 +240,20 @@ struct StripEpilogue {
         *reinterpret_cast<bf16x8*>(dst) = o;
       }
     }
-    // V^T [head][d][token]: 8 consecutive tokens of one channel per lane
+    // V^T [head][d][token]: 8 consecutive tokens of one channel per lane;
+    // four lanes cover the strip's 32 tokens (64 contiguous bytes)
     if (n0 + TN > 2 * hidden) {
       constexpr int IT = TN * 4 / 64;
 #pragma unroll
       for (int q = 0; q < IT; ++q) {
-        const int f = q * 64 + lane, col = f % TN, grp = f / TN;
+        const int col = q * 16 + (lane >> 2), grp = lane & 3;
         const int n = n0 + col;
         if (n < 2 * hidden) continue;
         float v[8];
 #pragma unroll
         for (int t = 0; t < 8; ++t) v[t] = strip[(grp * 8 + t) * LS + col];
         const float bias = ep.bias[n];
-        const int nn = n - 2 * hidden, head = nn / hd, dd = nn - head * hd;
+        const int nn = n - 2 * hidden, head = (int)__umulhi((unsigned)nn, ep.hd_magic), dd = nn - head * hd;
         bf16* vt = kvb + ntot * hidden + ((size_t)head * hd + dd) * ntot + ep.tok_offset;
         const int m = mr + grp * 8;
         const int b = m < M ? branch_of(m) : 0, tok = m - b * rpb;
@@ -587,15 +588,19 @@ static bool mfma_path_ok(const void* A, const void* W, int N, int K, int epi, co
     return false;
   if (epi == kEpiResidual) return aligned16(ep.out) && aligned16(ep.gate) && ep.gate_stride % 4 == 0;
   if (epi == kEpiQkv)
-    return aligned16(ep.q) && aligned16(ep.kv) && ep.head_dim % 8 == 0 && ep.kv_branch_stride % 8 == 0;
+    return aligned16(ep.q) && aligned16(ep.kv) && ep.head_dim % 8 == 0 && ep.kv_branch_stride % 8 == 0 &&
+           ep.hidden < 65536;
   return aligned16(ep.out);
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int S, int EPI>
-static void launch_tile(const void* A, const void* W, int M, int N, int K, const EpiParams& ep,
+static void launch_tile(const void* A, const void* W, int M, int N, int K, const EpiParams& ep0,
                         hipStream_t s) {
   const int tm = ceil_div(M, BM), tn = N / BN;
   constexpr int lds = S * GemmGeo<BM, BN, BK, WM, WN, S>::STAGE;
+  EpiParams ep = ep0;
+  // head = umulhi(channel, ceil(2^32 / head_dim)): exact for channels < 2^16
+  if (EPI == kEpiQkv) ep.hd_magic = (unsigned)((0x100000000ull + ep.head_dim - 1) / ep.head_dim);
   auto kern = gemm_bf16_kernel<BM, BN, BK, WM, WN, S, EPI>;
   static bool attr = [&] {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),

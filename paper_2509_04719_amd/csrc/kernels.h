@@ -24,6 +24,7 @@ struct EpiParams {
   int kv_tokens;              // token extent of the K/V destination
   int tok_offset;             // destination token of the first row
   int heads, hidden, head_dim;
+  unsigned hd_magic;          // set by the launcher: ceil(2^32 / head_dim)
 };
 
 // y = A W^T (+ epilogue).  A T [M][K], W T [N][K].
