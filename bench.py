@@ -36,6 +36,130 @@ PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 METRIC = "patch-step ms and TFLOP/s vs bf16 MFMA peak, DiT-XL/2 1024px, 1 GPU"
 
+# HBM traffic of the dominant kernel, from two rocprofv3 --pmc runs of
+# `bench.py --pmc-probe` (FETCH_SIZE, then WRITE_SIZE) turned into a report by
+# `bench.py --pmc-report`; valid only while the kernel's sources are unchanged.
+TRAFFIC_REPORT = os.path.join(ROOT, "profiles", "attention_xl1024_band40_traffic.md")
+KERNEL_SOURCES = {
+    "attention": ["paper_2509_04719_amd/csrc/k_attention.hip", "paper_2509_04719_amd/csrc/common.h",
+                  "paper_2509_04719_amd/csrc/kernels.h", "paper_2509_04719_amd/build.py"],
+}
+KERNEL_NAMES = {"attention": "attn_bf16_mfma_kernel"}
+# calibration: the scheduler-update kernel with no unconditional branch and no
+# noise reads x and eps and writes out, 4 bytes each per element
+CALIB_ELEMS = 64 << 20
+CALIB_NAME = "update_vec4_kernel"
+
+
+def kernel_source_hash(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(kernel: str):
+    """Bytes per launch from the committed counter report, or None when the
+    report is missing or the kernel's sources changed since it was taken."""
+    try:
+        with open(TRAFFIC_REPORT) as f:
+            kv = dict(l.strip()[2:].split(": ", 1) for l in f if l.startswith("- ") and ": " in l)
+    except OSError:
+        return None
+    if kv.get("kernel") != kernel or kv.get("source_sha256") != kernel_source_hash(kernel):
+        return None
+    return float(kv["hbm_bytes_per_launch"])
+
+
+def pmc_probe(a) -> int:
+    """Workload of the counter runs: the calibration stream, then the bench
+    step (warm-up and three timed-shape steps)."""
+    import numpy as np
+    import torch
+
+    from paper_2509_04719_amd import _lib as L
+    from paper_2509_04719_amd import schedule as psched
+    from seeded_inputs import configs, generate
+
+    dev = "cuda:0"
+    xs = torch.randn(CALIB_ELEMS, device=dev)
+    es = torch.randn(CALIB_ELEMS, device=dev)
+    os_ = torch.empty(CALIB_ELEMS, device=dev)
+    for _ in range(3):
+        L.scheduler_update(xs, es, None, 1.0, None, 0.9, 0.1, 0.0, os_)
+    torch.cuda.synchronize()
+    del xs, es, os_
+    cfg = configs.get(a.config)
+    rows = psched.band_rows(a.share, cfg.R)
+    t, tp = configs.headline_timestep_pair(cfg)
+    ctx = L.DiTStep(cfg, generate.make_weight_blob(cfg, 0))
+    x = torch.from_numpy(generate.make_latent(cfg, 0)).to(dev)
+    labels = generate.make_labels(cfg, 0)
+    kv = torch.from_numpy(generate.make_stale_kv(cfg, 0).view(np.int16)).to(dev).view(torch.bfloat16)
+    out = torch.empty((cfg.in_ch, rows * cfg.patch, cfg.latent), device=dev)
+    for _ in range(5):
+        ctx.step(x, 0, rows, t, tp, labels, cfg.cfg_scale, kv, 1, out)
+    torch.cuda.synchronize()
+    ctx.close()
+    print("pmc probe done", flush=True)
+    return 0
+
+
+def pmc_report(fetch_dir: str, write_dir: str, kernel: str = "attention") -> int:
+    """Summarise the two counter runs (FETCH_SIZE, WRITE_SIZE; KiB per
+    dispatch) as the traffic report bench.py reads."""
+    import csv
+    import glob
+
+    def per_dispatch(d, counter):
+        # {kernel key: {dispatch: (grid size, counter sum)}}; the calibration
+        # dispatches are the update launches with the largest grid (the steps
+        # launch the same kernel on the band)
+        vals = {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] != counter:
+                    continue
+                for key in (CALIB_NAME, KERNEL_NAMES[kernel]):
+                    if key in r["Kernel_Name"]:
+                        g, v = vals.setdefault(key, {}).get(r["Dispatch_Id"], (int(r["Grid_Size"]), 0.0))
+                        vals[key][r["Dispatch_Id"]] = (g, v + float(r["Counter_Value"]))
+        out = {}
+        for key, disp in vals.items():
+            gmax = max(g for g, _ in disp.values())
+            keep = [v for g, v in disp.values() if key != CALIB_NAME or g == gmax]
+            out[key] = sorted(keep)
+        return out
+
+    fetch = per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = per_dispatch(write_dir, "WRITE_SIZE")
+    med = lambda v: v[len(v) // 2]
+    calib_read_kib, calib_write_kib = 8 * CALIB_ELEMS / 1024, 4 * CALIB_ELEMS / 1024
+    fscale = calib_read_kib / med(fetch[CALIB_NAME])
+    wscale = calib_write_kib / med(write[CALIB_NAME])
+    k = KERNEL_NAMES[kernel]
+    fb = med(fetch[k]) * fscale * 1024
+    wb = med(write[k]) * wscale * 1024
+    print(f"# HBM traffic of the {kernel} kernel, DiT-XL/2 1024px band step (26 of 64 rows)\n")
+    print("Commands (repository root, on the GPU host):\n")
+    print("    rocprofv3 --pmc FETCH_SIZE -d <fetch_dir> -o pmc --output-format csv -- python3 bench.py --pmc-probe")
+    print("    rocprofv3 --pmc WRITE_SIZE -d <write_dir> -o pmc --output-format csv -- python3 bench.py --pmc-probe")
+    print("    python3 bench.py --pmc-report <fetch_dir> <write_dir>\n")
+    print(f"Calibration: `{CALIB_NAME}` over {CALIB_ELEMS} fp32 elements reads {8 * CALIB_ELEMS} B and writes "
+          f"{4 * CALIB_ELEMS} B; the counters read {med(fetch[CALIB_NAME]):.1f} KiB and "
+          f"{med(write[CALIB_NAME]):.1f} KiB per dispatch, so FETCH_SIZE is scaled by {fscale:.4f} and "
+          f"WRITE_SIZE by {wscale:.4f}.\n")
+    print(f"Per {kernel} dispatch (median of {len(fetch[k])} / {len(write[k])}): FETCH_SIZE "
+          f"{med(fetch[k]):.1f} KiB, WRITE_SIZE {med(write[k]):.1f} KiB.\n")
+    print(f"- kernel: {kernel}")
+    print(f"- source_sha256: {kernel_source_hash(kernel)}")
+    print(f"- fetch_bytes_per_launch: {fb:.0f}")
+    print(f"- write_bytes_per_launch: {wb:.0f}")
+    print(f"- hbm_bytes_per_launch: {fb + wb:.0f}")
+    return 0
+
 
 def step_flops(cfg, n_q: int) -> float:
     """Algorithmic FLOPs of one band step (band tokens only; nothing for stale rows)."""
@@ -228,7 +352,13 @@ def main(argv=None) -> int:
     ap.add_argument("--schedule", action="store_true",
                     help="time the whole sampler schedule of the band instead of one step "
                          "(the tiered schedule for configs that use it)")
+    ap.add_argument("--pmc-probe", action="store_true",
+                    help="run the workload of the HBM counter runs and exit")
+    ap.add_argument("--pmc-report", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the traffic report from two counter runs and exit")
     a = ap.parse_args(argv)
+    if a.pmc_report:
+        return pmc_report(*a.pmc_report)
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {a.gpus}).", file=sys.stderr)
@@ -244,6 +374,8 @@ def main(argv=None) -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
+    if a.pmc_probe:
+        return pmc_probe(a)
     dev = "cuda:0"
     cfg = configs.get(a.config)
     rows = psched.band_rows(a.share, cfg.R)
@@ -290,8 +422,11 @@ def main(argv=None) -> int:
     mfma_names = [k for k in ("qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm") if k in split]
     mfma_flops = sum(split[k]["flop_per_launch"] * split[k]["launches_per_step"] for k in mfma_names)
     mfma_ms = sum(split[k]["ms_per_step"] for k in mfma_names)
+    traffic = recorded_traffic(dom) if dom in KERNEL_SOURCES else None
     roofline = {"kernel": dom, "bound": "mfma", "achieved": d["tflops"], "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(d["tflops"] / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(d["tflops"] / PEAK_BF16_TFLOPS, 4),
+                "traffic": None if traffic is None else round(traffic),
+                "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated)",
                 "flop_per_launch": d["flop_per_launch"], "ms_per_launch": d["ms"],
                 "measured": "HIP events around each launch inside the timed steps"}
     print(f"# kernels: {json.dumps(split)}", flush=True)
