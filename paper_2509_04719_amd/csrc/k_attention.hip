@@ -280,6 +280,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   auto half = [&](auto next_c, int st, int sub, const f32x16& sc, const bf16x8(&kn)[NC],
                   f32x16& sn) {
     constexpr bool NEXT = decltype(next_c)::value;
+    // this half's V^T fragments, read early so the PV MFMAs do not wait on LDS
+    bf16x8 vfr[2][NT];
+#pragma unroll
+    for (int ci = 0; ci < 2; ++ci)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) vfr[ci][tt] = v_frag(st, tt, 2 * sub + ci);
     // online softmax over this lane's query column.  The running max is only
     // raised when some lane's max exceeds it by more than 8 (log2 units):
     // until then exp2(s - m_run) <= 2^8, exact in fp32 and in range for
@@ -326,7 +332,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     for (int ci = 0; ci < 2; ++ci)
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt)
-        o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(st, tt, 2 * sub + ci), pf[ci], o[tt], 0, 0, 0);
+        o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[ci][tt], pf[ci], o[tt], 0, 0, 0);
   };
 
   const int NIT = kv_len / BKV;
