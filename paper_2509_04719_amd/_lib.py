@@ -24,6 +24,7 @@ SYMBOLS = (
     "orch_last_error", "orch_op_layernorm_modulate", "orch_op_linear", "orch_op_qkv_projection",
     "orch_op_attention", "orch_op_conditioning", "orch_op_patch_embed", "orch_op_final_layer",
     "orch_attention_workspace_bytes", "orch_set_kernel_timing", "orch_kernel_times",
+    "orch_plan_devices",
 )
 KCLASSES = ("conditioning", "patch_embed", "layernorm", "qkv_gemm", "attention", "proj_gemm",
             "fc1_gemm", "fc2_gemm", "final_layer", "update")
@@ -76,6 +77,7 @@ def _load():
         "orch_op_conditioning": (i, [vp, i, C.POINTER(i), vp, vp]),
         "orch_op_patch_embed": (i, [vp, vp, i, i, vp, vp]),
         "orch_op_final_layer": (i, [vp, vp, i, i, vp, vp, vp]),
+        "orch_plan_devices": (i, [C.POINTER(d), i, i, i, d, d, i, C.POINTER(i), C.POINTER(i)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -113,6 +115,16 @@ def schedule_coefficients(cfg, t: int, t_prev: int, eta: float = 0.0):
     oc = config_from(cfg)
     check(lib.orch_schedule_coefficients(C.byref(oc), t, t_prev, eta, out))
     return out[0], out[1], out[2]
+
+
+def plan_devices(speeds, m_base, m_warmup, a, b, total_rows):
+    """(steps, rows) per device from the library's planner (host only)."""
+    n = len(speeds)
+    v = (C.c_double * n)(*[float(x) for x in speeds])
+    st = (C.c_int * n)()
+    rw = (C.c_int * n)()
+    check(lib.orch_plan_devices(v, n, m_base, m_warmup, float(a), float(b), total_rows, st, rw))
+    return list(st), list(rw)
 
 
 class DiTStep:

@@ -58,6 +58,11 @@ float bf16_bits_to_float(uint16_t v) {
 
 }  // namespace
 
+namespace orch_detail {
+// error reporting for the host-only entry points of other translation units
+int set_error(int code, const char* msg) { return fail(code, "%s", msg); }
+}  // namespace orch_detail
+
 struct orch_ctx {
   orch_dit_config cfg;
   int device = 0;

@@ -1,0 +1,63 @@
+// Device planning of the method, host only: temporal adaptation (Eq. (2),
+// tiered step counts with exclusion) and spatial adaptation (Eq. (3), patch
+// mending), turned into whole token rows.
+#include <cmath>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "../../include/orch.h"
+
+namespace orch_detail {
+int set_error(int code, const char* msg);
+}
+
+int orch_plan_devices(const double* speed, int n, int m_base, int m_warmup, double a, double b,
+                      int total_rows, int* steps_out, int* rows_out) {
+  using orch_detail::set_error;
+  if (!speed || !steps_out || !rows_out) return set_error(ORCH_EINVAL, "NULL argument");
+  if (n < 1 || total_rows < 1) return set_error(ORCH_EINVAL, "need n >= 1 and total_rows >= 1");
+  if (m_base < 1 || m_warmup < 0 || m_warmup > m_base)
+    return set_error(ORCH_EINVAL, "need m_base >= 1 and 0 <= m_warmup <= m_base");
+  if (!(0.0 < b && b < a && a < 1.0)) return set_error(ORCH_EINVAL, "need 0 < b < a < 1");
+  double vmax = 0.0;
+  for (int i = 0; i < n; ++i) {
+    if (!(speed[i] > 0.0) || !std::isfinite(speed[i]))
+      return set_error(ORCH_EINVAL, "speeds must be finite and > 0");
+    vmax = std::max(vmax, speed[i]);
+  }
+  // Eq. (2): full, reduced (M_base/2 + M_warmup/2) or excluded
+  std::vector<int> steps(n);
+  for (int i = 0; i < n; ++i) {
+    if (speed[i] > a * vmax) steps[i] = m_base;
+    else if (speed[i] > b * vmax) steps[i] = m_base / 2 + m_warmup / 2;
+    else steps[i] = 0;
+  }
+  // Eq. (3): share of device i = (v_i/M_i) / sum_j (v_j/M_j)
+  double tot = 0.0;
+  std::vector<double> rate(n, 0.0);
+  for (int i = 0; i < n; ++i)
+    if (steps[i]) tot += (rate[i] = speed[i] / steps[i]);
+  // whole rows by largest remainders (ties to the lower index)
+  std::vector<int> rows(n);
+  std::vector<double> frac(n);
+  int used = 0;
+  for (int i = 0; i < n; ++i) {
+    const double exact = rate[i] / tot * total_rows;
+    rows[i] = (int)std::floor(exact);
+    frac[i] = exact - rows[i];
+    used += rows[i];
+  }
+  for (int left = total_rows - used; left > 0; --left) {
+    int best = -1;
+    for (int i = 0; i < n; ++i)
+      if (steps[i] && (best < 0 || frac[i] > frac[best])) best = i;
+    ++rows[best];
+    frac[best] = -1.0;
+  }
+  for (int i = 0; i < n; ++i) {
+    steps_out[i] = steps[i];
+    rows_out[i] = rows[i];
+  }
+  return ORCH_OK;
+}

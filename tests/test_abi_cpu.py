@@ -77,3 +77,44 @@ def test_create_rejects_bad_config_without_gpu_work(orch_lib):
     rc = orch_lib.lib.orch_create(C.byref(bad), C.byref(h))
     assert rc == orch_lib.ORCH_EINVAL and not h.value
     assert "heads" in orch_lib.last_error()
+
+
+# ---- device planner (host only: Eq. (2), Eq. (3)) ------------------------
+
+from oracle import allocator as oal  # noqa: E402
+
+
+def test_library_plan_matches_oracle_exactly(orch_lib):
+    rng = np.random.default_rng(7)
+    for trial in range(300):
+        n = int(rng.integers(1, 9))
+        v = list(rng.uniform(0.05, 1.0, n))
+        a = float(rng.uniform(0.5, 0.9))
+        b = float(rng.uniform(0.05, a - 0.01))
+        mb = int(rng.integers(2, 120))
+        mw = int(rng.integers(0, mb + 1))
+        rows = int(rng.integers(1, 257))
+        got = orch_lib.plan_devices(v, mb, mw, a, b, rows)
+        want = oal.plan(v, mb, mw, a, b, rows)
+        assert got == (want[0], want[1]), (trial, v, a, b, mb, mw, rows)
+
+
+def test_library_plan_reproduces_quality_tables(orch_lib):
+    # two GPUs, 32 units, M_base 100, M_warmup 4, v = 1 - occupancy
+    assert orch_lib.plan_devices([1.0, 0.8], 100, 4, 0.75, 0.3, 32) == ([100, 100], [18, 14])
+    assert orch_lib.plan_devices([1.0, 0.6], 100, 4, 0.75, 0.3, 32) == ([100, 52], [15, 17])
+    assert orch_lib.plan_devices([0.65, 0.55], 100, 4, 0.75, 0.3, 32) == ([100, 100], [17, 15])
+    assert orch_lib.plan_devices([0.7, 0.5], 100, 4, 0.75, 0.3, 32) == ([100, 52], [13, 19])
+    assert orch_lib.plan_devices([1.0, 0.5], 50, 4, 0.75, 0.3, 32)[0] == [50, 27]
+
+
+@pytest.mark.parametrize("args,word", [
+    (([1.0, -0.5], 50, 4, 0.75, 0.3, 32), "speeds"),
+    (([1.0], 50, 60, 0.75, 0.3, 32), "m_warmup"),
+    (([1.0], 50, 4, 0.3, 0.75, 32), "0 < b < a < 1"),
+    (([1.0], 50, 4, 0.75, 0.3, 0), "total_rows"),
+])
+def test_library_plan_rejects_bad_arguments(orch_lib, args, word):
+    with pytest.raises(orch_lib.OrchError) as e:
+        orch_lib.plan_devices(*args)
+    assert e.value.code == orch_lib.ORCH_EINVAL and word in orch_lib.last_error()

@@ -1,0 +1,68 @@
+"""Pins of the device planner (Eq. (2), Eq. (3)) against the paper's tables."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import allocator as al
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "table1_patch_assignment.txt")
+
+
+def _table1():
+    rows = []
+    for line in open(GOLDEN):
+        if line.strip() and not line.startswith("#"):
+            rows.append(tuple(int(x) for x in line.split()))
+    return rows
+
+
+@pytest.mark.parametrize("row", _table1())
+def test_table1_assignments(row):
+    """Quality table: patch units and reduced tier from occupancies (v = 1 - rho)."""
+    o0, o1, p0, p1, red = row
+    v = [al.effective_speed(1.0, o0 / 100), al.effective_speed(1.0, o1 / 100)]
+    steps, rows = al.plan(v, 100, 4, a=0.75, b=0.3, total_rows=32)
+    assert rows == [p0, p1]
+    assert steps == [100, 52 if red else 100]
+
+
+@pytest.mark.parametrize("M_base,expect", [(100, 52), (50, 27)])
+def test_table2_step_counts(M_base, expect):
+    """Quality table II: a reduced device runs 100:52 and 50:27 steps (M_warmup = 4)."""
+    assert al.step_counts([1.0, 0.5], M_base, 4, a=0.75, b=0.3) == [M_base, expect]
+
+
+def test_thresholds_and_exclusion():
+    v = [1.0, 0.9, 0.75, 0.5, 0.3, 0.29]
+    steps = al.step_counts(v, 50, 10, a=0.75, b=0.3)
+    # a*vmax < v keeps M_base; b*vmax < v <= a*vmax reduced; v <= b*vmax excluded
+    assert steps == [50, 50, 30, 30, 0, 0]
+    steps, rows = al.plan(v, 50, 10, 0.75, 0.3, 64)
+    assert rows[4] == rows[5] == 0 and sum(rows) == 64
+
+
+def test_equal_devices_split_evenly():
+    steps, rows = al.plan([0.7] * 4, 50, 10, 0.75, 0.3, 64)
+    assert steps == [50] * 4 and rows == [16] * 4
+
+
+def test_mending_equalises_rate():
+    """Eq. (3): (v_i/M_i)/P_i is the same for every device (before rounding)."""
+    rng = np.random.default_rng(0)
+    v = list(rng.uniform(0.35, 1.0, 7))
+    steps = al.step_counts(v, 100, 4, 0.8, 0.3)
+    sh = al.patch_shares(v, steps)
+    r = [vi / m / s for vi, m, s in zip(v, steps, sh) if m]
+    assert np.allclose(r, r[0]) and abs(sum(sh) - 1) < 1e-12
+
+
+def test_whole_rows_largest_remainder():
+    assert al.whole_rows([0.5, 0.5], 5) == [3, 2]          # tie -> lower index
+    assert al.whole_rows([0.1, 0.2, 0.7], 10) == [1, 2, 7]
+    assert al.whole_rows([1 / 3] * 3, 64) == [22, 21, 21]
+    rng = np.random.default_rng(1)
+    for _ in range(200):
+        s = rng.dirichlet(np.ones(5))
+        r = al.whole_rows(list(s), 61)
+        assert sum(r) == 61 and all(abs(ri - si * 61) < 1 for ri, si in zip(r, s))
