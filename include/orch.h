@@ -109,6 +109,36 @@ int orch_patch_denoise_step(orch_ctx* ctx, const float* x_full, int row_begin, i
                             void* stale_kv, int refresh, const float* z, float eta,
                             float* out_eps, float* out_x_patch, void* hip_stream);
 
+/* Algorithm 1 on n_bands virtual devices, run one after another on this GPU:
+ * the whole sampler from x_{t_grid[0]} to the final latent, in place.
+ *   latent      device fp32 [in_ch][latent][latent]: the initial noise in,
+ *               the sample out.
+ *   row_splits  host [n_bands + 1]: device i owns token rows
+ *               [row_splits[i], row_splits[i+1]); 0 = row_splits[0] < ... <
+ *               row_splits[n_bands] = latent / patch.
+ *   tiers       host [n_bands]: 0 = every grid step, 1 = the reduced tier of
+ *               Eq. (2) (steps of two grid intervals after the warm-up).
+ *   t_grid      host [steps + 1]: strictly decreasing timesteps below T,
+ *               t_grid[steps] = -1.
+ *   warmup      1 <= warmup <= steps.
+ *   kv_a, kv_b  device, orch_stale_kv_bytes() each: the K/V buffer of the
+ *               last exchange and the one being filled; both are
+ *               overwritten.
+ * Warm-up steps are full-image steps (synchronous exchange): the buffer then
+ * holds every token's K/V of that step.  After the warm-up the grid is
+ * covered in sync intervals of two steps (one if a single step is left): each
+ * device reads the buffer of the interval's start for the other devices'
+ * tokens (its own are fresh); a tier-0 device runs t_m -> t_{m+1}, exchanging
+ * that step's K/V, then t_{m+1} -> t_{m+2} without exchange (Algorithm 1:
+ * no buffer update on odd offsets); a tier-1 device runs t_m -> t_{m+2} and
+ * exchanges.  At the interval's end the exchanged K/V become the buffer and
+ * the bands form the latent.  DDIM (eta = 0).  Errors: ORCH_EINVAL,
+ * ORCH_ENOWEIGHTS, ORCH_EHIP. */
+int orch_sample_patch_parallel(orch_ctx* ctx, float* latent, int n_bands, const int* row_splits,
+                               const int* tiers, const int* t_grid, int steps, int warmup,
+                               const int* labels, float cfg_scale, void* kv_a, void* kv_b,
+                               void* hip_stream);
+
 /* The fused guidance + scheduler update of §I, elementwise over n floats:
  *   eps = eps_uncond ? eps_uncond + g (eps_cond - eps_uncond) : eps_cond
  *   out = a x - b eps + c z          (z may be NULL when c == 0)

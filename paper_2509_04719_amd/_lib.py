@@ -24,7 +24,7 @@ SYMBOLS = (
     "orch_last_error", "orch_op_layernorm_modulate", "orch_op_linear", "orch_op_qkv_projection",
     "orch_op_attention", "orch_op_conditioning", "orch_op_patch_embed", "orch_op_final_layer",
     "orch_attention_workspace_bytes", "orch_set_kernel_timing", "orch_kernel_times",
-    "orch_plan_devices",
+    "orch_plan_devices", "orch_sample_patch_parallel",
 )
 KCLASSES = ("conditioning", "patch_embed", "layernorm", "qkv_gemm", "attention", "proj_gemm",
             "fc1_gemm", "fc2_gemm", "final_layer", "update")
@@ -78,6 +78,8 @@ def _load():
         "orch_op_patch_embed": (i, [vp, vp, i, i, vp, vp]),
         "orch_op_final_layer": (i, [vp, vp, i, i, vp, vp, vp]),
         "orch_plan_devices": (i, [C.POINTER(d), i, i, i, d, d, i, C.POINTER(i), C.POINTER(i)]),
+        "orch_sample_patch_parallel": (i, [vp, vp, i, C.POINTER(i), C.POINTER(i), C.POINTER(i), i, i,
+                                           C.POINTER(i), f, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -162,6 +164,18 @@ class DiTStep:
                                           lab, float(cfg_scale), _ptr(stale_kv), int(refresh),
                                           _ptr(z), float(eta), _ptr(out_eps), _ptr(out_x),
                                           _stream(stream)))
+
+    def sample_patch_parallel(self, latent, row_splits, tiers, t_grid, warmup, labels, cfg_scale,
+                              kv_a, kv_b, stream=None):
+        """Algorithm 1 on virtual devices (bands), in place on `latent`."""
+        n = len(tiers)
+        sp = (C.c_int * (n + 1))(*[int(v) for v in row_splits])
+        tr = (C.c_int * n)(*[int(v) for v in tiers])
+        tg = (C.c_int * len(t_grid))(*[int(v) for v in t_grid])
+        lab = (C.c_int * len(labels))(*[int(v) for v in labels])
+        check(lib.orch_sample_patch_parallel(self.handle, _ptr(latent), n, sp, tr, tg,
+                                             len(t_grid) - 1, int(warmup), lab, float(cfg_scale),
+                                             _ptr(kv_a), _ptr(kv_b), _stream(stream)))
 
     def set_kernel_timing(self, enable: bool):
         check(lib.orch_set_kernel_timing(self.handle, int(enable)))

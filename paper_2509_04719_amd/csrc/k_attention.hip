@@ -125,16 +125,19 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
                    (size_t)p.n_kv * H + (size_t)head * D * p.n_kv;
   const bf16* kf = ks;
   const bf16* vf = vs;
+  const int fn = nf > 0 ? p.fresh_n : p.n_kv;     // token extent of the fresh buffer
   if (nf > 0) {
-    kf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)head * nf * D;
-    vf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)nf * H +
-         (size_t)head * D * nf;
+    kf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs +
+         ((size_t)head * fn + p.fresh_off) * D;
+    vf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)fn * H +
+         (size_t)head * D * fn + p.fresh_off;
   }
   // buffer resources of this (branch, head): out-of-range reads return zero
   const __amdgpu_buffer_rsrc_t rks = buffer_rsrc(ks, (size_t)p.n_kv * D * 2);
   const __amdgpu_buffer_rsrc_t rvs = buffer_rsrc(vs, (size_t)p.n_kv * D * 2);
   const __amdgpu_buffer_rsrc_t rkf = buffer_rsrc(kf, (size_t)(nf > 0 ? nf : p.n_kv) * D * 2);
-  const __amdgpu_buffer_rsrc_t rvf = buffer_rsrc(vf, (size_t)(nf > 0 ? nf : p.n_kv) * D * 2);
+  const __amdgpu_buffer_rsrc_t rvf =
+      buffer_rsrc(vf, ((size_t)(D - 1) * fn + (nf > 0 ? nf : p.n_kv)) * 2);
 
   // this lane's query (B operand of S^T = K Q^T): Q[q][c*16 + 8h .. +8]
   const int qrow = min(q0 + wave * 32 + lc, p.n_q - 1);
@@ -204,7 +207,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
       const unsigned so = __builtin_amdgcn_readfirstlane((unsigned)(n0 - fb) * (kwave ? 2 * D : 2));
 #pragma unroll
       for (int i = 0; i < LPW; ++i) {
-        const unsigned o = kwave ? off[i] : off[i] - (unsigned)(vrow(i) * (p.n_kv - nf)) * 2u;
+        const unsigned o = kwave ? off[i] : off[i] - (unsigned)(vrow(i) * (p.n_kv - fn)) * 2u;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst_of(st, i), 16, o, so, 0, 0);
       }
     } else {
@@ -226,7 +229,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
           const int n = n0 + key;
           const bool fr = (unsigned)(n - fb) < (unsigned)nf;
           base = reinterpret_cast<const char*>(fr ? vf : vs);
-          bo = (unsigned)(fr ? d * nf + (n - fb) : d * p.n_kv + n) * 2u;
+          bo = (unsigned)(fr ? d * fn + (n - fb) : d * p.n_kv + n) * 2u;
         }
         __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)(base + bo), dst_of(st, i), 16, 0, 0);
       }
@@ -456,9 +459,10 @@ __global__ __launch_bounds__(64) void attn_simt_kernel(AttnParams p) {
   const T* kf = nullptr;
   const T* vf = nullptr;
   if (p.n_fresh > 0) {
-    kf = reinterpret_cast<const T*>(p.kv_fresh) + b * p.fresh_bs + (size_t)head * p.n_fresh * D;
-    vf = reinterpret_cast<const T*>(p.kv_fresh) + b * p.fresh_bs + (size_t)p.n_fresh * H +
-         (size_t)head * D * p.n_fresh;
+    kf = reinterpret_cast<const T*>(p.kv_fresh) + b * p.fresh_bs +
+         ((size_t)head * p.fresh_n + p.fresh_off) * D;
+    vf = reinterpret_cast<const T*>(p.kv_fresh) + b * p.fresh_bs + (size_t)p.fresh_n * H +
+         (size_t)head * D * p.fresh_n + p.fresh_off;
   }
   float qr[D], acc[D];
   const float scale = 1.0f / sqrtf((float)D);
@@ -481,7 +485,7 @@ __global__ __launch_bounds__(64) void attn_simt_kernel(AttnParams p) {
     l = l * a + e;
 #pragma unroll
     for (int d = 0; d < D; ++d) {
-      const float v = fresh ? to_f<T>(vf[(size_t)d * p.n_fresh + f]) : to_f<T>(vs[(size_t)d * p.n_kv + n]);
+      const float v = fresh ? to_f<T>(vf[(size_t)d * p.fresh_n + f]) : to_f<T>(vs[(size_t)d * p.n_kv + n]);
       acc[d] = fmaf(acc[d], a, e * v);
     }
     m = mn;
@@ -556,7 +560,8 @@ hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
   // time, all fresh or all stale)
   const bool aligned = p.fresh_begin % 8 == 0 && p.n_fresh % 8 == 0 && aligned16(p.q) &&
                        aligned16(p.kv_stale) && p.stale_bs % 8 == 0 &&
-                       (p.n_fresh == 0 || (aligned16(p.kv_fresh) && p.fresh_bs % 8 == 0));
+                       (p.n_fresh == 0 || (aligned16(p.kv_fresh) && p.fresh_bs % 8 == 0 &&
+                                           p.fresh_n % 8 == 0 && p.fresh_off % 8 == 0));
   if (attention_uses_mfma(p.d, p.n_kv, dtype) && aligned) {
     const int want = pick_splits(p.B, p.heads, p.n_q, p.n_kv);
     if (want > 1 && p.ws &&

@@ -392,8 +392,8 @@ __global__ __launch_bounds__(256) void update_vec4_kernel(const float* __restric
                                                           const float* __restrict__ eu, float g,
                                                           const float* __restrict__ z, int ldz,
                                                           float a, float b, float c,
-                                                          float* __restrict__ out, int rows,
-                                                          size_t cols4) {
+                                                          float* __restrict__ out, int ldo,
+                                                          int rows, size_t cols4) {
   const size_t total = (size_t)rows * cols4;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < total;
        i += (size_t)gridDim.x * 256) {
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(256) void update_vec4_kernel(const float* __restric
       o.z += c * zv.z;
       o.w += c * zv.w;
     }
-    reinterpret_cast<float4*>(out + r * cols4 * 4)[q] = o;
+    reinterpret_cast<float4*>(out + r * (size_t)ldo)[q] = o;
   }
 }
 
@@ -429,8 +429,8 @@ __global__ __launch_bounds__(256) void update_scalar_kernel(const float* __restr
                                                             const float* __restrict__ eu, float g,
                                                             const float* __restrict__ z, int ldz,
                                                             float a, float b, float c,
-                                                            float* __restrict__ out, int rows,
-                                                            size_t cols) {
+                                                            float* __restrict__ out, int ldo,
+                                                            int rows, size_t cols) {
   const size_t total = (size_t)rows * cols;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < total;
        i += (size_t)gridDim.x * 256) {
@@ -442,27 +442,27 @@ __global__ __launch_bounds__(256) void update_scalar_kernel(const float* __restr
     }
     float o = a * x[r * (size_t)ldx + q] - b * e;
     if (z) o += c * z[r * (size_t)ldz + q];
-    out[r * cols + q] = o;
+    out[r * (size_t)ldo + q] = o;
   }
 }
 
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 hipError_t launch_update(const float* x, int ldx, const float* ec, const float* eu, float g,
-                         const float* z, int ldz, float a, float b, float c, float* out, int rows,
-                         size_t cols, hipStream_t s) {
+                         const float* z, int ldz, float a, float b, float c, float* out, int ldo,
+                         int rows, size_t cols, hipStream_t s) {
   const size_t total = (size_t)rows * cols;
   if (total == 0) return hipSuccess;
-  const bool vec = cols % 4 == 0 && ldx % 4 == 0 && (!z || ldz % 4 == 0) && al16(x) && al16(ec) &&
-                   (!eu || al16(eu)) && (!z || al16(z)) && al16(out);
+  const bool vec = cols % 4 == 0 && ldx % 4 == 0 && ldo % 4 == 0 && (!z || ldz % 4 == 0) &&
+                   al16(x) && al16(ec) && (!eu || al16(eu)) && (!z || al16(z)) && al16(out);
   const size_t work = vec ? total / 4 : total;
   const int blocks = (int)std::min<size_t>((work + 255) / 256, 8192);
   if (vec)
     hipLaunchKernelGGL(update_vec4_kernel, dim3(blocks), dim3(256), 0, s, x, ldx, ec, eu, g, z,
-                       ldz, a, b, c, out, rows, cols / 4);
+                       ldz, a, b, c, out, ldo, rows, cols / 4);
   else
     hipLaunchKernelGGL(update_scalar_kernel, dim3(blocks), dim3(256), 0, s, x, ldx, ec, eu, g, z,
-                       ldz, a, b, c, out, rows, cols);
+                       ldz, a, b, c, out, ldo, rows, cols);
   return hipGetLastError();
 }
 

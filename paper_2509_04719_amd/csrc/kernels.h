@@ -45,6 +45,11 @@ struct AttnParams {
   const void* kv_fresh;       // T, branch stride fresh_bs; may be null when n_fresh == 0
   size_t fresh_bs;
   int fresh_begin, n_fresh;
+  // layout of the fresh buffer: token extent (K [heads][fresh_n][d], V^T at
+  // fresh_n*H as [heads][d][fresh_n]) and the index of token fresh_begin in
+  // it: (n_fresh, 0) for a compact band buffer, (n_kv, fresh_begin) when the
+  // fresh K/V sit in a buffer of the stale layout
+  int fresh_n, fresh_off;
   int B, heads, n_q, n_kv, d;
   void* out;                  // T [B][n_q][heads*d]
   // split-KV workspace (optional): fp32 partials, see attention_workspace_bytes
@@ -99,8 +104,9 @@ hipError_t launch_final_linear(const FinalParams& p, int dtype, hipStream_t stre
 
 // out = a x - b (eu + g (ec - eu)) + c z over a [rows][cols] region; x has
 // row stride ldx, z row stride ldz, the rest row stride cols.  eu, z nullable.
+// out row r at out + r * ldo (rows = channels of a band, or one flat row)
 hipError_t launch_update(const float* x, int ldx, const float* ec, const float* eu, float g,
-                         const float* z, int ldz, float a, float b, float c, float* out, int rows,
-                         size_t cols, hipStream_t stream);
+                         const float* z, int ldz, float a, float b, float c, float* out, int ldo,
+                         int rows, size_t cols, hipStream_t stream);
 
 }  // namespace orch

@@ -93,6 +93,7 @@ struct orch_ctx {
   float* eps = nullptr;
   void* attn_ws = nullptr;
   size_t attn_ws_bytes = 0;
+  float* lat[3] = {};   // latents of the patch-parallel sampler
 
   // per-kernel timing: event pairs recorded around each launch of a step
   struct Timing {
@@ -227,6 +228,8 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
   const size_t tokB = (size_t)x->B * x->n_kv;
   struct Part { size_t bytes; void** dst; };
   void *p_h, *p_u, *p_q, *p_kvf, *p_att, *p_mlp, *p_mod, *p_t1, *p_sc, *p_eps, *p_aws;
+  void* p_lat[3];
+  const size_t lat_bytes = (size_t)cfg->in_ch * cfg->latent * cfg->latent * 4;
   // split-KV partials: the largest need over every band height
   size_t aws = 0;
   for (int r = 1; r <= x->R; ++r)
@@ -239,7 +242,7 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
       {(size_t)x->B * x->n_mod * 4, &p_mod}, {(size_t)x->H * 4, &p_t1},
       {(size_t)x->B * x->H * 4, &p_sc},
       {(size_t)x->B * cfg->out_ch * cfg->latent * cfg->latent * 4, &p_eps},
-      {aws, &p_aws}};
+      {aws, &p_aws}, {lat_bytes, &p_lat[0]}, {lat_bytes, &p_lat[1]}, {lat_bytes, &p_lat[2]}};
   size_t total = 0;
   for (const Part& p : parts) total += (p.bytes + 255) / 256 * 256;
   hipError_t e = hipMalloc(&x->ws, total);
@@ -255,6 +258,7 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
   x->h = (float*)p_h; x->u = p_u; x->q = p_q; x->kvf = p_kvf; x->att = p_att; x->mlp = p_mlp;
   x->mod = (float*)p_mod; x->t1 = (float*)p_t1; x->sc = (float*)p_sc; x->eps = (float*)p_eps;
   x->attn_ws = aws ? p_aws : nullptr;
+  for (int i = 0; i < 3; ++i) x->lat[i] = (float*)p_lat[i];
   *out = x;
   return ORCH_OK;
 }
@@ -516,43 +520,22 @@ int run_final(orch_ctx* x, const float* h, int rb, int re, const float* mod, flo
 
 extern "C" {
 
-int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev,
-                            const int* labels, float cfg_scale, void* stale_kv, int refresh,
-                            const float* z, float eta, float* out_eps, float* out_x_patch,
-                            void* hip_stream) {
-  if (!x) return fail(ORCH_EINVAL, "ctx is NULL");
-  if (!x->loaded) return fail(ORCH_ENOWEIGHTS, "weights not loaded");
-  if (!x_full || !stale_kv || !out_x_patch) return fail(ORCH_EINVAL, "x_full, stale_kv and out_x_patch must be non-NULL");
-  if (rb < 0 || re <= rb || re > x->R) return fail(ORCH_EINVAL, "band [%d, %d) not within [0, %d)", rb, re, x->R);
-  if (t < 0 || t >= x->cfg.T || t_prev < -1 || t_prev >= t)
-    return fail(ORCH_EINVAL, "need 0 <= t < T and -1 <= t_prev < t (t=%d, t_prev=%d)", t, t_prev);
-  if (!(eta >= 0.0f) || !std::isfinite(eta)) return fail(ORCH_EINVAL, "eta must be finite and >= 0");
-  if (eta > 0.0f && !z) return fail(ORCH_EINVAL, "eta > 0 needs z");
-  if (!std::isfinite(cfg_scale)) return fail(ORCH_EINVAL, "cfg_scale must be finite");
-  int rc = check_labels(x, labels);
-  if (rc) return rc;
+namespace {
+
+// One executed step of one band, arguments already validated.  kv_in is
+// read for the tokens outside the band.  The band's fresh K/V go to kv_out
+// (buffer layout, band tokens only) when it is non-NULL -- kv_out == kv_in
+// is the in-place refresh -- else to the workspace.  The band of x_{t_prev}
+// is written at out_x, channel c at out_x + c * ldo.
+int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev,
+             const int* labels, float cfg_scale, void* kv_in, void* kv_out, const float* z,
+             float eta, float* out_eps, float* out_x, int ldo, hipStream_t s) {
   const orch_dit_config& c = x->cfg;
   const int p = c.patch;
   const int n_rows = re - rb;
   const int n_tok = n_rows * x->R;
   const size_t lat2 = (size_t)c.latent * c.latent;
-  const size_t x_bytes = c.in_ch * lat2 * 4;
-  const size_t out_bytes = (size_t)c.in_ch * n_rows * p * c.latent * 4;
-  const size_t eps_bytes = (size_t)x->B * c.out_ch * n_rows * p * c.latent * 4;
-  const size_t kv_bytes = orch_stale_kv_bytes(x);
-  if (ranges_overlap(out_x_patch, out_bytes, x_full, x_bytes) ||
-      ranges_overlap(out_x_patch, out_bytes, stale_kv, kv_bytes) ||
-      ranges_overlap(out_x_patch, out_bytes, out_eps, eps_bytes) ||
-      ranges_overlap(out_eps, eps_bytes, x_full, x_bytes) ||
-      ranges_overlap(out_eps, eps_bytes, stale_kv, kv_bytes))
-    return fail(ORCH_EINVAL, "output buffers overlap inputs");
-  if (((uintptr_t)x_full | (uintptr_t)stale_kv | (uintptr_t)out_x_patch | (uintptr_t)out_eps |
-       (uintptr_t)z) & 15)
-    return fail(ORCH_EINVAL, "device buffers must be 16-byte aligned");
-  rc = check_device(x);
-  if (rc) return rc;
-
-  hipStream_t s = (hipStream_t)hip_stream;
+  int rc;
   double abc[3];
   coefficients(c, t, t_prev, eta, abc);
   const int dt = c.dtype;
@@ -565,13 +548,14 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
   rc = run_patch_embed(x, x_full, rb, re, x->h, s);
   if (rc) return rc;
 
-  // K/V destination of the QKV epilogue: the buffer itself when refreshing
-  // (band tokens only), else the fresh workspace read by attention.
+  // K/V destination of the QKV epilogue: kv_out (band tokens only) when
+  // given, else the fresh workspace read by attention.
   const size_t stale_bs = (size_t)2 * x->n_kv * H;
   const size_t fresh_bs = (size_t)2 * n_tok * H;
   for (int l = 0; l < x->L; ++l) {
     const float* mb = x->mod + (size_t)6 * H * l;  // shift1 scale1 gate1 shift2 scale2 gate2
-    void* layer_kv = (char*)stale_kv + (size_t)l * B * stale_bs * es;
+    void* layer_kv = (char*)kv_in + (size_t)l * B * stale_bs * es;
+    void* layer_out = kv_out ? (char*)kv_out + (size_t)l * B * stale_bs * es : nullptr;
 
     {
       KernelTimer kt(x, ORCH_KCLASS_LAYERNORM, s);
@@ -583,8 +567,8 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
     eq.rows_per_batch = n_tok;
     eq.q = x->q;
     eq.heads = x->heads; eq.hidden = H; eq.head_dim = x->d;
-    if (refresh) {
-      eq.kv = layer_kv; eq.kv_branch_stride = stale_bs; eq.kv_tokens = x->n_kv; eq.tok_offset = rb * x->R;
+    if (layer_out) {
+      eq.kv = layer_out; eq.kv_branch_stride = stale_bs; eq.kv_tokens = x->n_kv; eq.tok_offset = rb * x->R;
     } else {
       eq.kv = x->kvf; eq.kv_branch_stride = fresh_bs; eq.kv_tokens = n_tok; eq.tok_offset = 0;
     }
@@ -595,8 +579,16 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
 
     AttnParams ap{};
     ap.q = x->q; ap.kv_stale = layer_kv; ap.stale_bs = stale_bs;
-    ap.kv_fresh = refresh ? nullptr : x->kvf; ap.fresh_bs = fresh_bs;
-    ap.fresh_begin = refresh ? 0 : rb * x->R; ap.n_fresh = refresh ? 0 : n_tok;
+    if (layer_out == layer_kv) {        // refreshed in place: every key in one buffer
+      ap.kv_fresh = nullptr; ap.fresh_bs = 0; ap.fresh_begin = 0; ap.n_fresh = 0;
+      ap.fresh_n = 0; ap.fresh_off = 0;
+    } else if (layer_out) {             // band keys in kv_out, at their own tokens
+      ap.kv_fresh = layer_out; ap.fresh_bs = stale_bs; ap.fresh_begin = rb * x->R;
+      ap.n_fresh = n_tok; ap.fresh_n = x->n_kv; ap.fresh_off = rb * x->R;
+    } else {                            // band keys in the compact workspace
+      ap.kv_fresh = x->kvf; ap.fresh_bs = fresh_bs; ap.fresh_begin = rb * x->R;
+      ap.n_fresh = n_tok; ap.fresh_n = n_tok; ap.fresh_off = 0;
+    }
     ap.B = B; ap.heads = x->heads; ap.n_q = n_tok; ap.n_kv = x->n_kv; ap.d = x->d; ap.out = x->att;
     ap.ws = x->attn_ws; ap.ws_bytes = x->attn_ws_bytes;
     {
@@ -645,10 +637,134 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
   {
     KernelTimer kt(x, ORCH_KCLASS_UPDATE, s);
     HIP_TRY(launch_update(xb, (int)lat2, ec, eu, cfg_scale, abc[2] != 0.0 ? zb : nullptr, (int)lat2,
-                          (float)abc[0], (float)abc[1], (float)abc[2], out_x_patch, c.in_ch,
+                          (float)abc[0], (float)abc[1], (float)abc[2], out_x, ldo, c.in_ch,
                           band_cols, s),
             "update launch");
   }
+  return ORCH_OK;
+}
+
+}  // namespace
+
+int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev,
+                            const int* labels, float cfg_scale, void* stale_kv, int refresh,
+                            const float* z, float eta, float* out_eps, float* out_x_patch,
+                            void* hip_stream) {
+  if (!x) return fail(ORCH_EINVAL, "ctx is NULL");
+  if (!x->loaded) return fail(ORCH_ENOWEIGHTS, "weights not loaded");
+  if (!x_full || !stale_kv || !out_x_patch) return fail(ORCH_EINVAL, "x_full, stale_kv and out_x_patch must be non-NULL");
+  if (rb < 0 || re <= rb || re > x->R) return fail(ORCH_EINVAL, "band [%d, %d) not within [0, %d)", rb, re, x->R);
+  if (t < 0 || t >= x->cfg.T || t_prev < -1 || t_prev >= t)
+    return fail(ORCH_EINVAL, "need 0 <= t < T and -1 <= t_prev < t (t=%d, t_prev=%d)", t, t_prev);
+  if (!(eta >= 0.0f) || !std::isfinite(eta)) return fail(ORCH_EINVAL, "eta must be finite and >= 0");
+  if (eta > 0.0f && !z) return fail(ORCH_EINVAL, "eta > 0 needs z");
+  if (!std::isfinite(cfg_scale)) return fail(ORCH_EINVAL, "cfg_scale must be finite");
+  int rc = check_labels(x, labels);
+  if (rc) return rc;
+  const orch_dit_config& c = x->cfg;
+  const int p = c.patch;
+  const int n_rows = re - rb;
+  const size_t lat2 = (size_t)c.latent * c.latent;
+  const size_t x_bytes = c.in_ch * lat2 * 4;
+  const size_t out_bytes = (size_t)c.in_ch * n_rows * p * c.latent * 4;
+  const size_t eps_bytes = (size_t)x->B * c.out_ch * n_rows * p * c.latent * 4;
+  const size_t kv_bytes = orch_stale_kv_bytes(x);
+  if (ranges_overlap(out_x_patch, out_bytes, x_full, x_bytes) ||
+      ranges_overlap(out_x_patch, out_bytes, stale_kv, kv_bytes) ||
+      ranges_overlap(out_x_patch, out_bytes, out_eps, eps_bytes) ||
+      ranges_overlap(out_eps, eps_bytes, x_full, x_bytes) ||
+      ranges_overlap(out_eps, eps_bytes, stale_kv, kv_bytes))
+    return fail(ORCH_EINVAL, "output buffers overlap inputs");
+  if (((uintptr_t)x_full | (uintptr_t)stale_kv | (uintptr_t)out_x_patch | (uintptr_t)out_eps |
+       (uintptr_t)z) & 15)
+    return fail(ORCH_EINVAL, "device buffers must be 16-byte aligned");
+  rc = check_device(x);
+  if (rc) return rc;
+
+  return run_step(x, x_full, rb, re, t, t_prev, labels, cfg_scale, stale_kv,
+                  refresh ? stale_kv : nullptr, z, eta, out_eps, out_x_patch,
+                  n_rows * p * c.latent, (hipStream_t)hip_stream);
+}
+
+int orch_sample_patch_parallel(orch_ctx* x, float* latent, int n_bands, const int* row_splits,
+                                const int* tiers, const int* t_grid, int steps, int warmup,
+                                const int* labels, float cfg_scale, void* kv_a, void* kv_b,
+                                void* hip_stream) {
+  if (!x) return fail(ORCH_EINVAL, "ctx is NULL");
+  if (!x->loaded) return fail(ORCH_ENOWEIGHTS, "weights not loaded");
+  if (!latent || !row_splits || !tiers || !t_grid || !kv_a || !kv_b)
+    return fail(ORCH_EINVAL, "NULL argument");
+  if (n_bands < 1) return fail(ORCH_EINVAL, "need n_bands >= 1");
+  if (row_splits[0] != 0 || row_splits[n_bands] != x->R)
+    return fail(ORCH_EINVAL, "row_splits must run from 0 to %d", x->R);
+  for (int i = 0; i < n_bands; ++i) {
+    if (row_splits[i + 1] <= row_splits[i]) return fail(ORCH_EINVAL, "row_splits must increase");
+    if (tiers[i] != 0 && tiers[i] != 1) return fail(ORCH_EINVAL, "tiers must be 0 or 1");
+  }
+  if (steps < 1 || warmup < 1 || warmup > steps)
+    return fail(ORCH_EINVAL, "need steps >= 1 and 1 <= warmup <= steps");
+  if (t_grid[steps] != -1) return fail(ORCH_EINVAL, "t_grid[steps] must be -1");
+  for (int m = 0; m < steps; ++m)
+    if (t_grid[m] >= x->cfg.T || t_grid[m] <= t_grid[m + 1])
+      return fail(ORCH_EINVAL, "t_grid must decrease from below T to -1");
+  if (!std::isfinite(cfg_scale)) return fail(ORCH_EINVAL, "cfg_scale must be finite");
+  int rc = check_labels(x, labels);
+  if (rc) return rc;
+  const orch_dit_config& c = x->cfg;
+  const size_t lat2 = (size_t)c.latent * c.latent;
+  const size_t lat_bytes = c.in_ch * lat2 * 4;
+  const size_t kv_bytes = orch_stale_kv_bytes(x);
+  if (ranges_overlap(kv_a, kv_bytes, kv_b, kv_bytes) ||
+      ranges_overlap(latent, lat_bytes, kv_a, kv_bytes) ||
+      ranges_overlap(latent, lat_bytes, kv_b, kv_bytes))
+    return fail(ORCH_EINVAL, "latent and the two K/V buffers must not overlap");
+  if (((uintptr_t)latent | (uintptr_t)kv_a | (uintptr_t)kv_b) & 15)
+    return fail(ORCH_EINVAL, "device buffers must be 16-byte aligned");
+  rc = check_device(x);
+  if (rc) return rc;
+
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int p = c.patch;
+  float* xc = x->lat[0];   // latent at the current grid point
+  float* xm = x->lat[1];   // a full-tier band after its first half-step
+  float* xn = x->lat[2];   // latent at the interval's end
+  void* bc = kv_a;         // buffer as of the last exchange
+  void* bn = kv_b;         // exchanged K/V of the running interval
+  HIP_TRY(hipMemcpyAsync(xc, latent, lat_bytes, hipMemcpyDeviceToDevice, s), "latent copy");
+  // warm-up: synchronous exchange inside the step = the full-image step; the
+  // buffer then holds that step's K/V of every token
+  for (int m = 0; m < warmup; ++m) {
+    rc = run_step(x, xc, 0, x->R, t_grid[m], t_grid[m + 1], labels, cfg_scale, bc, bc, nullptr,
+                  0.0f, nullptr, xn, (int)lat2, s);
+    if (rc) return rc;
+    std::swap(xc, xn);
+  }
+  // sync intervals of two grid steps (one if a single step is left): every
+  // device reads the buffer of the interval's start; a full-tier device
+  // exchanges its first half-step's K/V and keeps its second's, a
+  // reduced-tier device takes the double step and exchanges its K/V
+  for (int m = warmup; m < steps;) {
+    const int m2 = std::min(m + 2, steps);
+    for (int i = 0; i < n_bands; ++i) {
+      const int rb = row_splits[i], re = row_splits[i + 1];
+      const size_t off = (size_t)rb * p * c.latent;
+      if (tiers[i] == 0 && m2 == m + 2) {
+        rc = run_step(x, xc, rb, re, t_grid[m], t_grid[m + 1], labels, cfg_scale, bc, bn,
+                      nullptr, 0.0f, nullptr, xm + off, (int)lat2, s);
+        if (rc) return rc;
+        rc = run_step(x, xm, rb, re, t_grid[m + 1], t_grid[m + 2], labels, cfg_scale, bc,
+                      nullptr, nullptr, 0.0f, nullptr, xn + off, (int)lat2, s);
+      } else {
+        rc = run_step(x, xc, rb, re, t_grid[m], t_grid[m2], labels, cfg_scale, bc, bn, nullptr,
+                      0.0f, nullptr, xn + off, (int)lat2, s);
+      }
+      if (rc) return rc;
+    }
+    std::swap(xc, xn);
+    std::swap(bc, bn);
+    m = m2;
+  }
+  HIP_TRY(hipMemcpyAsync(latent, xc, lat_bytes, hipMemcpyDeviceToDevice, s), "latent copy");
   return ORCH_OK;
 }
 
@@ -664,7 +780,7 @@ int orch_scheduler_update(const float* xin, const float* eps_cond, const float* 
   hipError_t pending = hipGetLastError();
   if (pending != hipSuccess) return hip_fail(pending, "earlier asynchronous error");
   HIP_TRY(launch_update(xin, 0, eps_cond, eps_uncond, cfg_scale, c != 0.0 ? z : nullptr, 0, (float)a,
-                        (float)b, (float)c, out, 1, n, (hipStream_t)hip_stream),
+                        (float)b, (float)c, out, 0, 1, n, (hipStream_t)hip_stream),
           "update launch");
   return ORCH_OK;
 }
@@ -746,6 +862,7 @@ int orch_op_attention(const void* q, const void* kv_stale, size_t stale_bs, cons
   ap.fresh_bs = fresh_bs; ap.fresh_begin = fresh_begin; ap.n_fresh = n_fresh; ap.B = B;
   ap.heads = heads; ap.n_q = n_q; ap.n_kv = n_kv; ap.d = head_dim; ap.out = out;
   ap.ws = workspace; ap.ws_bytes = workspace ? workspace_bytes : 0;
+  ap.fresh_n = n_fresh; ap.fresh_off = 0;
   HIP_TRY(launch_attention(ap, dtype, (hipStream_t)hip_stream), "attention launch");
   return ORCH_OK;
 }
