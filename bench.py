@@ -336,6 +336,66 @@ def run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q) -> int:
     return 0
 
 
+def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
+    """Algorithm 1 on virtual devices: the device planner (Eq. (2), Eq. (3))
+    turns the device speeds into step counts and token rows, then the
+    library's sampler runs every band's whole trajectory on this GPU."""
+    import torch
+
+    from paper_2509_04719_amd import _lib as L
+    from paper_2509_04719_amd import schedule as psched
+
+    speeds = [float(v) for v in a.speeds.split(",")]
+    steps, rows = L.plan_devices(speeds, a.m_base, a.m_warmup, a.thr_a, a.thr_b, cfg.R)
+    splits, tiers = [0], []
+    for st, r in zip(steps, rows):
+        if st and r:
+            splits.append(splits[-1] + r)
+            tiers.append(0 if st == a.m_base else 1)
+    grid = psched.grid_desc(cfg.T, a.m_base)
+    # algorithmic work: warm-up steps over every row, then per interval one
+    # band step per tier-1 band and two per tier-0 band (one at the end if a
+    # single grid step is left)
+    flops = a.m_warmup * step_flops(cfg, cfg.n_q(cfg.R))
+    m = a.m_warmup
+    while m < a.m_base:
+        two = m + 2 <= a.m_base
+        for i, tier in enumerate(tiers):
+            n = 2 if (tier == 0 and two) else 1
+            flops += n * step_flops(cfg, cfg.n_q(splits[i + 1] - splits[i]))
+        m += 2 if two else 1
+    n_kv = ctx.stale_kv_bytes()
+    kv_a = torch.empty(n_kv, dtype=torch.uint8, device=x.device)
+    kv_b = torch.empty(n_kv, dtype=torch.uint8, device=x.device)
+    lat = x.clone()
+
+    def sample():
+        lat.copy_(x)
+        ctx.sample_patch_parallel(lat, splits, tiers, grid, a.m_warmup, labels, cfg.cfg_scale,
+                                  kv_a, kv_b)
+
+    sample()                                           # warm-up pass
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(a.steps):
+        sample()
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / a.steps
+    res = {"metric": "ms per image of the patch-parallel sampler on virtual devices", "value": round(ms, 2),
+           "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": 1, "higher_is_better": False,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": f"{cfg.name}: {len(tiers)} virtual devices, speeds {speeds}, "
+                                  f"M_base {a.m_base}, M_warmup {a.m_warmup}, a {a.thr_a}, b {a.thr_b}",
+                      "device_steps": steps, "device_rows": rows, "row_splits": splits,
+                      "tiers": tiers},
+           "tflops": round(flops / ms / 1e9, 1)}
+    print(json.dumps(res), flush=True)
+    ctx.close()
+    return 0
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -352,6 +412,14 @@ def main(argv=None) -> int:
     ap.add_argument("--schedule", action="store_true",
                     help="time the whole sampler schedule of the band instead of one step "
                          "(the tiered schedule for configs that use it)")
+    ap.add_argument("--virtual-devices", action="store_true",
+                    help="time the whole patch-parallel sampler over virtual devices planned "
+                         "from --speeds (Algorithm 1 on this GPU)")
+    ap.add_argument("--speeds", default="1.0,1.0,0.6,0.6")
+    ap.add_argument("--m-base", type=int, default=50)
+    ap.add_argument("--m-warmup", type=int, default=10)
+    ap.add_argument("--thr-a", type=float, default=0.75)
+    ap.add_argument("--thr-b", type=float, default=0.3)
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run the workload of the HBM counter runs and exit")
     ap.add_argument("--pmc-report", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -399,6 +467,8 @@ def main(argv=None) -> int:
 
     if a.schedule:
         return run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q)
+    if a.virtual_devices:
+        return run_virtual_devices(a, cfg, ctx, x, labels)
 
     for _ in range(a.warmup):
         one()
