@@ -48,6 +48,13 @@ __device__ __forceinline__ float gelu_tanh_f(float x) {
 
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// max of v over lanes l and l ^ 32, on the VALU (v_permlane32_swap: lane l
+// of the first result holds v[l & 31], of the second v[l | 32])
+__device__ __forceinline__ float max_xhalf(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // ---------------------------------------------------------------------------
 // Direct-to-LDS loads, counter waits and compile-time loops (MFMA kernels).
 #define ORCH_LDS __attribute__((address_space(3)))

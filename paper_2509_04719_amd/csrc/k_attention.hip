@@ -280,15 +280,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   // tile in stage st.  With NEXT, the MFMAs of the next half's scores (K
   // fragments kn, result sn) are issued between the exponentials; then
   // O^T += V^T P^T over the half's two 16-key chunks.
-  auto half = [&](auto next_c, int st, int sub, const f32x16& sc, const bf16x8(&kn)[NC],
-                  f32x16& sn) {
+  auto half = [&](auto next_c, int st, int sub, const f32x16& sc, int nst, int nsub, f32x16& sn) {
     constexpr bool NEXT = decltype(next_c)::value;
-    // this half's V^T fragments, read early so the PV MFMAs do not wait on LDS
-    bf16x8 vfr[2][NT];
-#pragma unroll
-    for (int ci = 0; ci < 2; ++ci)
-#pragma unroll
-      for (int tt = 0; tt < NT; ++tt) vfr[ci][tt] = v_frag(st, tt, 2 * sub + ci);
     // online softmax over this lane's query column.  The running max is only
     // raised when some lane's max exceeds it by more than 8 (log2 units):
     // until then exp2(s - m_run) <= 2^8, exact in fp32 and in range for
@@ -297,7 +290,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     float mx = fmaxf(sc[0], sc[1]);
 #pragma unroll
     for (int r = 2; r < 16; r += 2) mx = fmaxf(mx, fmaxf(sc[r], sc[r + 1]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale;
+    mx = max_xhalf(mx) * scale;   // VALU swap: no LDS round trip behind the fragment reads
     float alpha = 1.0f;
     if (__any(mx > m_run + 8.0f)) {
       const float m_new = fmaxf(m_run, mx);
@@ -308,6 +301,17 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[tt][r] *= alpha;
     }
+    // the next half's K fragments and this half's V^T fragments, issued after
+    // the rescale branch (a branch join makes the compiler wait for every LDS
+    // read in flight) and consumed behind the exponentials
+    bf16x8 kn[NC];
+    if constexpr (NEXT) k_frags(nst, nsub, kn);
+    bf16x8 vfr[2][NT];
+#pragma unroll
+    for (int ci = 0; ci < 2; ++ci)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) vfr[ci][tt] = v_frag(st, tt, 2 * sub + ci);
+    __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of their uses
     if constexpr (NEXT) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) sn[r] = 0.0f;
@@ -348,7 +352,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   // scores ping-pong between s0 (first halves) and s1 (second halves)
   f32x16 s0, s1;
   bf16x8 kn[NC];
-  k_frags(0, 0, kn);
+  k_frags(0, 0, kn);   // the first half's scores
 #pragma unroll
   for (int r = 0; r < 16; ++r) s0[r] = 0.0f;
 #pragma unroll
@@ -357,20 +361,17 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   int t = 0;
   for (; t + 1 < NIT; ++t) {
     const int st = t % NSTAGE;
-    k_frags(st, 1, kn);
-    half(std::true_type{}, st, 0, s0, kn, s1);
+    half(std::true_type{}, st, 0, s0, st, 1, s1);
     // tile t+1 resident; stage (t-1) % NSTAGE is free for tile t+3
     wait_tiles(t + 2 < NIT ? 1 : 0);
     lds_barrier();
     if (t + NSTAGE - 1 < NIT) issue(kv0 + (t + NSTAGE - 1) * BKV, (t + NSTAGE - 1) % NSTAGE);
-    k_frags((t + 1) % NSTAGE, 0, kn);
-    half(std::true_type{}, st, 1, s1, kn, s0);
+    half(std::true_type{}, st, 1, s1, (t + 1) % NSTAGE, 0, s0);
   }
   {
     const int st = t % NSTAGE;
-    k_frags(st, 1, kn);
-    half(std::true_type{}, st, 0, s0, kn, s1);
-    half(std::false_type{}, st, 1, s1, kn, s0);
+    half(std::true_type{}, st, 0, s0, st, 1, s1);
+    half(std::false_type{}, st, 1, s1, 0, 0, s0);
   }
 
   // softmax denominator: the ones row D of O^T (register 4*((D%32)/8) + D%4
