@@ -149,16 +149,55 @@ struct StripEpilogue {
     return b;
   }
 
+  // GELU, tanh form, as y * sigmoid(2u): 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)),
+  // u = sqrt(2/pi) (y + 0.044715 y^3), with e^(-2u) = exp2(y (c0 + c1 y^2))
   __device__ __forceinline__ static float act(float y) {
     if (EPI != kEpiGelu) return y;
-    const float u = 0.7978845608028654f * (y + 0.044715f * y * y * y);
-    const float e = __expf(2.0f * u);
-    const float th = 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
-    return 0.5f * y * (1.0f + th);
+    constexpr float c0 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+    constexpr float c1 = c0 * 0.044715f;
+    const float e = __builtin_amdgcn_exp2f(y * fmaf(c1, y * y, c0));
+    return y * __builtin_amdgcn_rcpf(1.0f + e);
+  }
+
+  // Operands of the epilogue loaded before the main loop, so their latency
+  // hides behind the MFMAs: the bias of each store chunk, and for the gated
+  // residual of one-strip tiles the fp32 h and gate rows as well.
+  static constexpr int SIT = 32 * (TN / 8) / 64;       // store chunks per lane per strip
+  static constexpr int RIT = 32 * (TN / 4) / 64;       // residual chunks per lane per strip
+  static constexpr bool PRE_H = EPI == kEpiResidual && FM == 1 && RIT <= 8;
+  struct Pre {
+    f32x4 b[(EPI == kEpiStore || EPI == kEpiGelu) ? SIT : 1][2];
+    f32x4 h[PRE_H ? RIT : 1], g[PRE_H ? RIT : 1], rb[PRE_H ? RIT : 1];
+  };
+
+  __device__ __forceinline__ void prefetch(Pre& pre, int lane, int m0, int n0) const {
+    if constexpr (EPI == kEpiStore || EPI == kEpiGelu) {
+      constexpr int CH = TN / 8;
+#pragma unroll
+      for (int q = 0; q < SIT; ++q) {
+        const int n = n0 + ((q * 64 + lane) % CH) * 8;
+        pre.b[q][0] = *reinterpret_cast<const f32x4*>(ep.bias + n);
+        pre.b[q][1] = *reinterpret_cast<const f32x4*>(ep.bias + n + 4);
+      }
+    }
+    if constexpr (PRE_H) {
+      constexpr int CH = TN / 4;
+      const float* hb = reinterpret_cast<const float*>(ep.out);
+#pragma unroll
+      for (int q = 0; q < RIT; ++q) {
+        const int f = q * 64 + lane, m = m0 + f / CH, n = n0 + (f % CH) * 4;
+        const bool in = m < M;
+        const int mm = in ? m : M - 1;
+        pre.h[q] = *reinterpret_cast<const f32x4*>(hb + (size_t)mm * N + n);
+        pre.g[q] = *reinterpret_cast<const f32x4*>(ep.gate + (size_t)branch_of(mm) * ep.gate_stride + n);
+        pre.rb[q] = *reinterpret_cast<const f32x4*>(ep.bias + n);
+      }
+    }
   }
 
   // rows [mr, mr + 32) x columns [n0, n0 + TN) of C, staged in strip
-  __device__ __forceinline__ void rows_store(const float* strip, int lane, int mr, int n0) const {
+  __device__ __forceinline__ void rows_store(const float* strip, int lane, int mr, int n0,
+                                             const Pre& pre) const {
     constexpr int CH = TN / 8, IT = 32 * CH / 64;
     bf16* out = reinterpret_cast<bf16*>(ep.out);
 #pragma unroll
@@ -168,8 +207,8 @@ struct StripEpilogue {
       const f32x4 x0 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8);
       const f32x4 x1 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8 + 4);
       if (m < M) {
-        const f32x4 b0 = *reinterpret_cast<const f32x4*>(ep.bias + n);
-        const f32x4 b1 = *reinterpret_cast<const f32x4*>(ep.bias + n + 4);
+        const f32x4 b0 = pre.b[q][0];
+        const f32x4 b1 = pre.b[q][1];
         bf16x8 o;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -181,26 +220,34 @@ struct StripEpilogue {
     }
   }
 
-  __device__ __forceinline__ void rows_residual(const float* strip, int lane, int mr, int n0) const {
+  __device__ __forceinline__ void rows_residual(const float* strip, int lane, int mr, int n0,
+                                                const Pre& pre) const {
     constexpr int CH = TN / 4, IT = 32 * CH / 64;
     float* hb = reinterpret_cast<float*>(ep.out);
     f32x4 x[IT], hv[IT];
-    // all loads first: the stores below may alias them as far as the
-    // compiler knows, so this keeps one round trip per strip
+    // all loads first (or prefetched): the stores below may alias them as far
+    // as the compiler knows, so this keeps at most one round trip per strip
 #pragma unroll
     for (int q = 0; q < IT; ++q) {
       const int f = q * 64 + lane, row = f / CH, c = f % CH;
       const int m = mr + row, n = n0 + c * 4;
       x[q] = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 4);
-      hv[q] = m < M ? *reinterpret_cast<const f32x4*>(hb + (size_t)m * N + n) : f32x4{0, 0, 0, 0};
+      if constexpr (PRE_H) hv[q] = pre.h[q];
+      else hv[q] = m < M ? *reinterpret_cast<const f32x4*>(hb + (size_t)m * N + n) : f32x4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int q = 0; q < IT; ++q) {
       const int f = q * 64 + lane, row = f / CH, c = f % CH;
       const int m = mr + row, n = n0 + c * 4;
       if (m < M) {
-        const f32x4 g = *reinterpret_cast<const f32x4*>(ep.gate + (size_t)branch_of(m) * ep.gate_stride + n);
-        const f32x4 b = *reinterpret_cast<const f32x4*>(ep.bias + n);
+        f32x4 g, b;
+        if constexpr (PRE_H) {
+          g = pre.g[q];
+          b = pre.rb[q];
+        } else {
+          g = *reinterpret_cast<const f32x4*>(ep.gate + (size_t)branch_of(m) * ep.gate_stride + n);
+          b = *reinterpret_cast<const f32x4*>(ep.bias + n);
+        }
         f32x4 y;
 #pragma unroll
         for (int r = 0; r < 4; ++r) y[r] = hv[q][r] + g[r] * (x[q][r] + b[r]);
@@ -279,7 +326,7 @@ struct StripEpilogue {
 
   // the wave's tile: rows [m0, m0 + 32 FM), columns [n0, n0 + TN)
   __device__ __forceinline__ void run(const f32x16 (&acc)[FM][FN], float* strip, int lane, int m0,
-                                      int n0) const {
+                                      int n0, const Pre& pre) const {
     const int lr = lane & 31, h = lane >> 5;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -289,8 +336,8 @@ struct StripEpilogue {
         for (int g = 0; g < 4; ++g)
           *reinterpret_cast<f32x4*>(strip + lr * LS + j * 32 + 8 * g + 4 * h) =
               f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-      if constexpr (EPI == kEpiStore || EPI == kEpiGelu) rows_store(strip, lane, m0 + 32 * i, n0);
-      else if constexpr (EPI == kEpiResidual) rows_residual(strip, lane, m0 + 32 * i, n0);
+      if constexpr (EPI == kEpiStore || EPI == kEpiGelu) rows_store(strip, lane, m0 + 32 * i, n0, pre);
+      else if constexpr (EPI == kEpiResidual) rows_residual(strip, lane, m0 + 32 * i, n0, pre);
       else rows_qkv(strip, lane, m0 + 32 * i, n0);
     }
   }
@@ -444,6 +491,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(const bf16* __r
     });
   };
 
+  // epilogue operands first: the oldest loads, covered by the main loop
+  using E = StripEpilogue<FM, FN, EPI>;
+  const E epi{ep, M, N};
+  typename E::Pre pre;
+  epi.prefetch(pre, lane, m0 + wm * G::TM, n0 + wn * G::TN);
+
 #pragma unroll
   for (int s = 0; s < S - 1; ++s) static_for<0, LPT>([&](auto jc) { dma(jc, s, s); });
   int kt = 0;
@@ -462,11 +515,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(const bf16* __r
   wait_vmcnt<0>(); lds_barrier(); compute(kt % S, std::false_type{}, 0, 0);
 
   // epilogue: the stage buffers become per-wave staging strips
-  using E = StripEpilogue<FM, FN, EPI>;
   static_assert(G::NW * E::BYTES <= S * G::STAGE, "epilogue staging fits the stage buffers");
   lds_barrier();
-  const E epi{ep, M, N};
-  epi.run(acc, reinterpret_cast<float*>(smem + wave * E::BYTES), lane, m0 + wm * G::TM, n0 + wn * G::TN);
+  epi.run(acc, reinterpret_cast<float*>(smem + wave * E::BYTES), lane, m0 + wm * G::TM, n0 + wn * G::TN,
+          pre);
 }
 
 // ---------------------------------------------------------------------------
