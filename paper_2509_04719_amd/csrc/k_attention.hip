@@ -101,57 +101,20 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5;
   const int lc = lane & 31;
-  // Workgroups go round-robin over the 8 XCDs; the ones of XCD x take the
-  // x-th contiguous eighth of the (branch, head, split, query tile) order, so
-  // the query tiles that read the same K/V share one L2.
+  // Work units: key tile k (64 keys) of query tile qt (128 queries) of
+  // (branch, head), in the order (b, head, qt, k); workgroup w takes units
+  // [w * per, (w + 1) * per).  Workgroups go round-robin over the 8 XCDs;
+  // the ones of XCD x take the x-th contiguous eighth of the workers, so the
+  // query tiles that read the same K/V share one L2.
   const int n_qt = (p.n_q + BQ - 1) / BQ;
+  const int nkt = p.n_kv / BKV;                   // key tiles (launcher: n_kv % BKV == 0)
+  const int units = n_qt * p.heads * p.B * nkt;
   const int T = gridDim.x;
-  int lb = blockIdx.x;
-  if (lb < T / 8 * 8) lb = (lb & 7) * (T / 8) + (lb >> 3);
-  const int qt = lb % n_qt;
-  const int split = (lb / n_qt) % p.splits;       // key split of this workgroup
-  const int pair = lb / (n_qt * p.splits);
-  const int head = pair % p.heads, b = pair / p.heads;
-  const int q0 = qt * BQ;
+  int w = blockIdx.x;
+  if (w < T / 8 * 8) w = (w & 7) * __builtin_amdgcn_readfirstlane(T / 8) + (w >> 3);
+  const int u_begin = w * p.per, u_end = min(u_begin + p.per, units);
   const int H = p.heads * D;
-  const int kv_len = p.n_kv / p.splits;           // multiple of BKV (launcher)
-  const int kv0 = split * kv_len;
   const int fb = p.fresh_begin, nf = p.n_fresh;
-
-  const bf16* qbase = reinterpret_cast<const bf16*>(p.q) + ((size_t)b * p.heads + head) * p.n_q * D;
-  const bf16* ks = reinterpret_cast<const bf16*>(p.kv_stale) + b * p.stale_bs +
-                   (size_t)head * p.n_kv * D;
-  const bf16* vs = reinterpret_cast<const bf16*>(p.kv_stale) + b * p.stale_bs +
-                   (size_t)p.n_kv * H + (size_t)head * D * p.n_kv;
-  const bf16* kf = ks;
-  const bf16* vf = vs;
-  const int fn = nf > 0 ? p.fresh_n : p.n_kv;     // token extent of the fresh buffer
-  if (nf > 0) {
-    kf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs +
-         ((size_t)head * fn + p.fresh_off) * D;
-    vf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)fn * H +
-         (size_t)head * D * fn + p.fresh_off;
-  }
-  // buffer resources of this (branch, head): out-of-range reads return zero
-  const __amdgpu_buffer_rsrc_t rks = buffer_rsrc(ks, (size_t)p.n_kv * D * 2);
-  const __amdgpu_buffer_rsrc_t rvs = buffer_rsrc(vs, (size_t)p.n_kv * D * 2);
-  const __amdgpu_buffer_rsrc_t rkf = buffer_rsrc(kf, (size_t)(nf > 0 ? nf : p.n_kv) * D * 2);
-  const __amdgpu_buffer_rsrc_t rvf =
-      buffer_rsrc(vf, ((size_t)(D - 1) * fn + (nf > 0 ? nf : p.n_kv)) * 2);
-
-  // this lane's query (B operand of S^T = K Q^T): Q[q][c*16 + 8h .. +8]
-  const int qrow = min(q0 + wave * 32 + lc, p.n_q - 1);
-  bf16x8 qf[NC];
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int d0 = c * 16 + h * 8;
-    if (d0 < D) {
-      qf[c] = *reinterpret_cast<const bf16x8*>(qbase + (size_t)qrow * D + d0);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)0.0f;
-    }
-  }
 
   // constant LDS (never written by the tile loads): 16 zero bytes after the
   // K rows of every stage, read against zero Q padding by the last chunk of
@@ -194,6 +157,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     if (j >= nload) return (ORCH_LDS void*)(smem + G::DUMMY_OFF);
     return (ORCH_LDS void*)(smem + st * G::STAGE + (kwave ? 0 : G::K_SPAN) + j * 1024);
   };
+  // state of the current segment's (branch, head): K/V bases, their buffer
+  // resources (out-of-range reads return zero), this lane's Q fragments
+  const int fn = nf > 0 ? p.fresh_n : p.n_kv;     // token extent of the fresh buffer
+  const bf16 *ks, *vs, *kf, *vf;
+  __amdgpu_buffer_rsrc_t rks, rvs, rkf, rvf;
+  bf16x8 qf[NC];
   auto issue = [&](int n0, int st) {
     const bool all_stale = n0 + BKV <= fb || n0 >= fb + nf;
     const bool all_fresh = n0 >= fb && n0 + BKV <= fb + nf;
@@ -255,12 +224,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   const bool last_in_pad = (NT - 1) * 32 + lc >= D;   // row of the last O^T tile is padding
 
   const float scale = 1.4426950408889634f / sqrtf((float)D);  // log2(e) / sqrt(d)
-  float m_run = -1e30f, l_run = 0.0f;
+  float m_run, l_run;
   f32x16 o[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
 
   // K fragments of half `sub` (keys [32 sub, +32)) of the tile in stage st
   auto k_frags = [&](int st, int sub, bf16x8(&kf_)[NC]) {
@@ -276,172 +241,284 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     return *reinterpret_cast<const bf16x8*>(src);
   };
 
-  // One 32-key half of a tile: scores sc = S^T of keys [32 sub, +32) of the
-  // tile in stage st.  With NEXT, the MFMAs of the next half's scores (K
-  // fragments kn, result sn) are issued between the exponentials; then
-  // O^T += V^T P^T over the half's two 16-key chunks.
-  auto half = [&](auto next_c, int st, int sub, const f32x16& sc, int nst, int nsub, f32x16& sn) {
+  // One 32-key half of the stream of key tiles.  sc: S^T of keys [32 sub,
+  // +32) of the tile in stage st.  Its exponentials are interleaved with the
+  // MFMAs of the next half's scores (NEXT: K fragments of stage nst, half
+  // nsub, into sn) and of the previous half's O^T += V^T P^T (probabilities
+  // pp, V^T of stage pst, half psub), so a wave keeps its matrix core busy
+  // through the softmax.  This half's probabilities go to pc.
+  auto step = [&](auto next_c, int st, int sub, const f32x16& sc, int nst, int nsub, f32x16& sn,
+                  int pst, int psub, bf16x8(&pp)[2], bf16x8(&pc)[2]) {
     constexpr bool NEXT = decltype(next_c)::value;
-    // online softmax over this lane's query column.  The running max is only
-    // raised when some lane's max exceeds it by more than 8 (log2 units):
-    // until then exp2(s - m_run) <= 2^8, exact in fp32 and in range for
-    // bf16, and O and the denominator keep a common scale, so O is rarely
-    // rescaled.
+    // online softmax over this lane's query column.  The running max is a
+    // whole number, raised only when some lane's max exceeds it by more than
+    // 8 (log2 units): until then exp2(s - m_run) <= 2^8, exact in fp32 and in
+    // range for bf16, so O is rarely rescaled; when it is, by a power of two,
+    // which scales the previous half's pending probabilities exactly too.
+    // the fragment reads go first, in order of use; the max below covers
+    // their latency
+    bf16x8 vp[2][NT];
+#pragma unroll
+    for (int ci = 0; ci < 2; ++ci)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) vp[ci][tt] = v_frag(pst, tt, 2 * psub + ci);
+    bf16x8 kn[NC];
+    if constexpr (NEXT) k_frags(nst, nsub, kn);
     float mx = fmaxf(sc[0], sc[1]);
 #pragma unroll
     for (int r = 2; r < 16; r += 2) mx = fmaxf(mx, fmaxf(sc[r], sc[r + 1]));
     mx = max_xhalf(mx) * scale;   // VALU swap: no LDS round trip behind the fragment reads
     float alpha = 1.0f;
-    if (__any(mx > m_run + 8.0f)) {
-      const float m_new = fmaxf(m_run, mx);
-      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    if (__builtin_expect(__any(mx > m_run + 8.0f), 0)) {
+      const float m_new = fmaxf(m_run, ceilf(mx));
+      alpha = ldexpf(1.0f, (int)fmaxf(m_run - m_new, -160.0f));
       m_run = m_new;
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[tt][r] *= alpha;
+#pragma unroll
+      for (int ci = 0; ci < 2; ++ci)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pp[ci][e] = (bf16)((float)pp[ci][e] * alpha);
     }
-    // the next half's K fragments and this half's V^T fragments, issued after
-    // the rescale branch (a branch join makes the compiler wait for every LDS
-    // read in flight) and consumed behind the exponentials
-    bf16x8 kn[NC];
-    if constexpr (NEXT) k_frags(nst, nsub, kn);
-    bf16x8 vfr[2][NT];
-#pragma unroll
-    for (int ci = 0; ci < 2; ++ci)
-#pragma unroll
-      for (int tt = 0; tt < NT; ++tt) vfr[ci][tt] = v_frag(st, tt, 2 * sub + ci);
-    __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of their uses
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (NEXT) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) sn[r] = 0.0f;
     }
     float psum = 0.0f;
-    bf16x8 pf[2];
+    // per 16-key chunk ci: NM MFMAs (PV and S alternating, PV first) in
+    // groups, each followed by its share of the chunk's 4 pairs of
+    // exponentials; a scheduling fence after each group keeps the order
     static_for<0, 2>([&](auto cc) {
       constexpr int ci = decltype(cc)::value;
-      if constexpr (NEXT) {
+      constexpr int c0 = ci * NC / 2, c1 = (ci + 1) * NC / 2;
+      constexpr int NSM = NEXT ? c1 - c0 : 0, NM = NSM + NT, NB = cmin(NSM, NT);
+      static_for<0, NM>([&](auto gc) {
+        constexpr int g = decltype(gc)::value;
+        constexpr bool pv = g < 2 * NB ? g % 2 == 0 : NT > NSM;
+        constexpr int idx = g < 2 * NB ? g / 2 : g - NB;
+        if constexpr (pv)
+          o[idx] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[ci][idx], pp[ci], o[idx], 0, 0, 0);
+        else
+          sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c0 + idx], qf[c0 + idx], sn, 0, 0, 0);
+        static_for<g * 4 / NM, (g + 1) * 4 / NM>([&](auto pc_) {
+          constexpr int pr = decltype(pc_)::value;
 #pragma unroll
-        for (int c = ci * NC / 2; c < (ci + 1) * NC / 2; ++c)
-          sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], sn, 0, 0, 0);
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int r = 4 * (2 * ci + (e >> 2)) + (e & 3);
-        const float pv = __builtin_amdgcn_exp2f(fmaf(sc[r], scale, -m_run));
-        if constexpr (!G::ONES) psum += pv;
-        pf[ci][e] = (bf16)pv;
-      }
+          for (int e = 2 * pr; e < 2 * pr + 2; ++e) {
+            const int r = 4 * (2 * ci + (e >> 2)) + (e & 3);
+            const float pv_ = __builtin_amdgcn_exp2f(fmaf(sc[r], scale, -m_run));
+            if constexpr (!G::ONES) psum += pv_;
+            pc[ci][e] = (bf16)pv_;
+          }
+        });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      // the probabilities are consumed one half later (by the next step or
+      // after the loop); this empty use keeps their exponentials here, between
+      // the MFMAs, instead of sunk into the next block
+      asm volatile("" ::"v"(pc[ci]));
     });
     if constexpr (!G::ONES) l_run = l_run * alpha + psum;
-    // chunk-major, so consecutive MFMAs accumulate into different O^T tiles
+  };
+
+  // segments: key tiles [a, bnd) of query tile `tile`, in unit order
+  // (the divisions run on the VALU; readfirstlane keeps the segment's
+  // indices, and the loop control built on them, in SGPRs)
+  for (int u = u_begin; u < u_end;) {
+    const int tile = __builtin_amdgcn_readfirstlane(u / nkt), a = u - tile * nkt;
+    const int bnd = min(nkt, a + (u_end - u));
+    const bool first = u == u_begin;
+    u += bnd - a;
+    const int pair = __builtin_amdgcn_readfirstlane(tile / n_qt), qt = tile - pair * n_qt;
+    const int b = __builtin_amdgcn_readfirstlane(pair / p.heads), head = pair - b * p.heads;
+    const int q0 = qt * BQ, kv0 = a * BKV, NIT = bnd - a;
+    if (!first) lds_barrier();   // every wave is done with the previous segment's stages
+    const bf16* qbase = reinterpret_cast<const bf16*>(p.q) + ((size_t)b * p.heads + head) * p.n_q * D;
+    ks = reinterpret_cast<const bf16*>(p.kv_stale) + b * p.stale_bs + (size_t)head * p.n_kv * D;
+    vs = reinterpret_cast<const bf16*>(p.kv_stale) + b * p.stale_bs + (size_t)p.n_kv * H +
+         (size_t)head * D * p.n_kv;
+    kf = ks;
+    vf = vs;
+    if (nf > 0) {
+      kf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + ((size_t)head * fn + p.fresh_off) * D;
+      vf = reinterpret_cast<const bf16*>(p.kv_fresh) + b * p.fresh_bs + (size_t)fn * H +
+           (size_t)head * D * fn + p.fresh_off;
+    }
+    rks = buffer_rsrc(ks, (size_t)p.n_kv * D * 2);
+    rvs = buffer_rsrc(vs, (size_t)p.n_kv * D * 2);
+    rkf = buffer_rsrc(kf, (size_t)(nf > 0 ? nf : p.n_kv) * D * 2);
+    rvf = buffer_rsrc(vf, ((size_t)(D - 1) * fn + (nf > 0 ? nf : p.n_kv)) * 2);
+    // this lane's query (B operand of S^T = K Q^T): Q[q][c*16 + 8h .. +8]
+    const int qrow = min(q0 + wave * 32 + lc, p.n_q - 1);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int d0 = c * 16 + h * 8;
+      if (d0 < D) {
+        qf[c] = *reinterpret_cast<const bf16x8*>(qbase + (size_t)qrow * D + d0);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)0.0f;
+      }
+    }
+    m_run = -1e30f;
+    l_run = 0.0f;
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[tt][r] = 0.0f;
+
+#pragma unroll
+    for (int s = 0; s < NSTAGE - 1; ++s)
+      if (s < NIT) issue(kv0 + s * BKV, s);
+    wait_tiles(min(NIT - 1, NSTAGE - 2));
+    lds_barrier();
+
+    // scores ping-pong between s0 (first halves) and s1 (second halves)
+    f32x16 s0, s1;
+    bf16x8 kn[NC];
+    k_frags(0, 0, kn);   // the first half's scores
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s0[r] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], s0, 0, 0, 0);
+
+    // probabilities of the previous and the current half, ping-pong; the
+    // first half's "previous" is zero against resident V^T rows
+    bf16x8 pa[2], pb[2];
 #pragma unroll
     for (int ci = 0; ci < 2; ++ci)
 #pragma unroll
-      for (int tt = 0; tt < NT; ++tt)
-        o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[ci][tt], pf[ci], o[tt], 0, 0, 0);
-  };
-
-  const int NIT = kv_len / BKV;
+      for (int e = 0; e < 8; ++e) pa[ci][e] = (bf16)0.0f;
+    int t = 0;
+    for (; t + 1 < NIT; ++t) {
+      const int st = t % NSTAGE;
+      const int pst = t == 0 ? st : (t + NSTAGE - 1) % NSTAGE;
+      step(std::true_type{}, st, 0, s0, st, 1, s1, pst, t == 0 ? 0 : 1, pa, pb);
+      // tile t+1 resident; stage (t-1) % NSTAGE is free for tile t+3
+      wait_tiles(t + 2 < NIT ? 1 : 0);
+      lds_barrier();
+      if (t + NSTAGE - 1 < NIT) issue(kv0 + (t + NSTAGE - 1) * BKV, (t + NSTAGE - 1) % NSTAGE);
+      step(std::true_type{}, st, 1, s1, (t + 1) % NSTAGE, 0, s0, st, 0, pb, pa);
+    }
+    {
+      const int st = t % NSTAGE;
+      const int pst = t == 0 ? st : (t + NSTAGE - 1) % NSTAGE;
+      step(std::true_type{}, st, 0, s0, st, 1, s1, pst, t == 0 ? 0 : 1, pa, pb);
+      step(std::false_type{}, st, 1, s1, 0, 0, s0, st, 0, pb, pa);
+      // the last half's PV
+      bf16x8 vp[2][NT];
 #pragma unroll
-  for (int s = 0; s < NSTAGE - 1; ++s)
-    if (s < NIT) issue(kv0 + s * BKV, s);
-  wait_tiles(min(NIT - 1, NSTAGE - 2));
-  lds_barrier();
-
-  // scores ping-pong between s0 (first halves) and s1 (second halves)
-  f32x16 s0, s1;
-  bf16x8 kn[NC];
-  k_frags(0, 0, kn);   // the first half's scores
+      for (int ci = 0; ci < 2; ++ci)
 #pragma unroll
-  for (int r = 0; r < 16; ++r) s0[r] = 0.0f;
+        for (int tt = 0; tt < NT; ++tt) vp[ci][tt] = v_frag(st, tt, 2 + ci);
 #pragma unroll
-  for (int c = 0; c < NC; ++c) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], s0, 0, 0, 0);
+      for (int ci = 0; ci < 2; ++ci)
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+          o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[ci][tt], pa[ci], o[tt], 0, 0, 0);
+    }
 
-  int t = 0;
-  for (; t + 1 < NIT; ++t) {
-    const int st = t % NSTAGE;
-    half(std::true_type{}, st, 0, s0, st, 1, s1);
-    // tile t+1 resident; stage (t-1) % NSTAGE is free for tile t+3
-    wait_tiles(t + 2 < NIT ? 1 : 0);
-    lds_barrier();
-    if (t + NSTAGE - 1 < NIT) issue(kv0 + (t + NSTAGE - 1) * BKV, (t + NSTAGE - 1) % NSTAGE);
-    half(std::true_type{}, st, 1, s1, (t + 1) % NSTAGE, 0, s0);
-  }
-  {
-    const int st = t % NSTAGE;
-    half(std::true_type{}, st, 0, s0, st, 1, s1);
-    half(std::false_type{}, st, 1, s1, 0, 0, s0);
-  }
-
-  // softmax denominator: the ones row D of O^T (register 4*((D%32)/8) + D%4
-  // of tile D/32 on the h == 0 lanes), or the running sum
-  float l;
-  if constexpr (G::ONES) {
-    constexpr int TR = D / 32, RR = 4 * ((D % 32) / 8) + (D % 4);
-    static_assert(((D % 32) / 4) % 2 == 0, "ones row on the h == 0 half");
-    l = __shfl(o[TR][RR], lc, kWave);
-  } else {
-    l = l_run + __shfl_xor(l_run, 32, kWave);
-  }
-  const int q = q0 + wave * 32 + lc;
-  if (p.splits > 1) {
-    // partial result of this key split: unnormalised O, running max and sum
+    // softmax denominator: the ones row D of O^T (register 4*((D%32)/8) + D%4
+    // of tile D/32 on the h == 0 lanes), or the running sum
+    float l;
+    if constexpr (G::ONES) {
+      constexpr int TR = D / 32, RR = 4 * ((D % 32) / 8) + (D % 4);
+      static_assert(((D % 32) / 4) % 2 == 0, "ones row on the h == 0 half");
+      l = __shfl(o[TR][RR], lc, kWave);
+    } else {
+      l = l_run + __shfl_xor(l_run, 32, kWave);
+    }
+    // a whole query tile goes to the output; the part of a cut one to this
+    // workgroup's slot (2w: its first segment, 2w + 1: its last) as O_s / l_s
+    // in bf16 with (max, sum), for the merge
+    const int ql = wave * 32 + lc, q = q0 + ql;
+    const bool whole = a == 0 && bnd == nkt;
+    const int slot = 2 * w + (first ? 0 : 1);
+    const float inv = 1.0f / l;
     if (q < p.n_q) {
-      float* orow = p.part_o + (((size_t)split * p.B + b) * p.n_q + q) * H + head * D;
+      bf16* orow = whole ? reinterpret_cast<bf16*>(p.out) + ((size_t)b * p.n_q + q) * H + head * D
+                         : reinterpret_cast<bf16*>(p.part_o) + ((size_t)slot * BQ + ql) * D;
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int d = t * 32 + 8 * g + 4 * h;
-          if (d < D)
-            *reinterpret_cast<float4*>(orow + d) =
-                make_float4(o[t][4 * g], o[t][4 * g + 1], o[t][4 * g + 2], o[t][4 * g + 3]);
+          if (d < D) {
+            bf16x4 v;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[t][4 * g + j] * inv);
+            *reinterpret_cast<bf16x4*>(orow + d) = v;
+          }
         }
-      if (h == 0)
-        p.part_ml[(((size_t)split * p.B + b) * p.heads + head) * p.n_q + q] = make_float2(m_run, l);
+      if (!whole && h == 0) p.part_ml[(size_t)slot * BQ + ql] = make_float2(m_run, l);
     }
-    return;
-  }
-  const float inv = 1.0f / l;
-  if (q < p.n_q) {
-    bf16* orow = reinterpret_cast<bf16*>(p.out) + ((size_t)b * p.n_q + q) * H + head * D;
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int d = t * 32 + 8 * g + 4 * h;
-        if (d < D) {
-          bf16x4 v;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[t][4 * g + j] * inv);
-          *reinterpret_cast<bf16x4*>(orow + d) = v;
-        }
-      }
   }
 #endif
 }
 
-// Combine of the key splits: O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s
-// (m = max_s m_s, all in the log2 domain of the kernel above).
-__global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
-  const int H = p.heads * p.d;
-  const size_t row = blockIdx.y;                 // b * n_q + q
-  const int col = blockIdx.x * 256 + threadIdx.x;
-  if (col >= H) return;
-  const int b = (int)(row / p.n_q), q = (int)(row - (size_t)b * p.n_q);
-  const int head = col / p.d;
-  float m = -1e30f;
-  for (int s = 0; s < p.splits; ++s)
-    m = fmaxf(m, p.part_ml[(((size_t)s * p.B + b) * p.heads + head) * p.n_q + q].x);
-  float num = 0.0f, den = 0.0f;
-  for (int s = 0; s < p.splits; ++s) {
-    const float2 ml = p.part_ml[(((size_t)s * p.B + b) * p.heads + head) * p.n_q + q];
-    const float w = __builtin_amdgcn_exp2f(ml.x - m);
-    num += w * p.part_o[((size_t)s * p.B * p.n_q + row) * H + col];
-    den += w * ml.y;
+// Merge of the parts of the query tiles cut between workgroups.  Part s
+// holds O_s / l_s with its running max m_s and sum l_s (log2 domain of the
+// kernel above); O = sum_s 2^(m_s - m) l_s (O_s / l_s) / sum_s 2^(m_s - m) l_s
+// with m = max_s m_s.  One thread per 8 channels of a query; grid (chunk
+// groups, query tiles).  The parts are taken four at a time with their loads
+// issued together (a tile is cut into two or three parts in the common
+// case), merged online.  Tiles computed whole return at once.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+  using namespace mfma_attn;
+  constexpr int CPQ = D / 8;                       // 16-byte chunks per query
+  const int nkt = p.n_kv / BKV, n_qt = (p.n_q + BQ - 1) / BQ;
+  const int tile = blockIdx.y;
+  const int w0 = tile * nkt / p.per, w1 = (tile * nkt + nkt - 1) / p.per;
+  if (w0 == w1) return;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  const int ql = i / CPQ, c = i - ql * CPQ;
+  const int qt = tile % n_qt, pair = tile / n_qt;
+  const int q = qt * BQ + ql;
+  if (ql >= BQ || q >= p.n_q) return;
+  const int head = pair % p.heads, b = pair / p.heads;
+  const bf16* part = reinterpret_cast<const bf16*>(p.part_o);
+  float m = -1e30f, den = 0.0f, num[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int wb = w0; wb <= w1; wb += 4) {
+    float2 ml[4];
+    bf16x8 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int w = wb + k;
+      if (w <= w1) {
+        const int slot = 2 * w + (w * p.per / nkt == tile ? 0 : 1);
+        ml[k] = p.part_ml[(size_t)slot * BQ + ql];
+        v[k] = *reinterpret_cast<const bf16x8*>(part + ((size_t)slot * BQ + ql) * D + c * 8);
+      } else {
+        ml[k] = make_float2(-1e30f, 0.0f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[k][e] = (bf16)0.0f;
+      }
+    }
+    float mc = m;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mc = fmaxf(mc, ml[k].x);
+    const float f = __builtin_amdgcn_exp2f(m - mc);
+    m = mc;
+    den *= f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) num[e] *= f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float wt = __builtin_amdgcn_exp2f(ml[k].x - m) * ml[k].y;
+      den += wt;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) num[e] = fmaf(wt, (float)v[k][e], num[e]);
+    }
   }
-  reinterpret_cast<bf16*>(p.out)[row * H + col] = (bf16)(num / den);
+  const float inv = 1.0f / den;
+  bf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (bf16)(num[e] * inv);
+  *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(p.out) + ((size_t)b * p.n_q + q) * p.heads * D +
+                             head * D + c * 8) = r;
 }
 
 // ---------------------------------------------------------------------------
@@ -517,25 +594,33 @@ static hipError_t launch_simt(const AttnParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Key splits: the largest power of two (<= 8) that keeps the workgroup count
-// within two per CU (512) and at least 4 key tiles per split.
-static int pick_splits(int B, int heads, int n_q, int n_kv) {
-  const int wg = ceil_div(n_q, mfma_attn::BQ) * heads * B;
-  const int tiles = n_kv / mfma_attn::BKV;
-  int s = 1;
-  while (s < 8 && wg * s * 2 <= 512 && tiles % (2 * s) == 0 && tiles / (2 * s) >= 4) s *= 2;
-  return s;
-}
+// Work plan.  Units are (branch, head, query tile, key tile).  Whole query
+// tiles per workgroup leave CUs idle when the tile count is not close to a
+// multiple of 512 (two workgroups per CU); with a workspace, every workgroup
+// takes per = ceil(units / 512) units instead, cutting query tiles between
+// workgroups, when that shortens the longest workgroup by more than 10% (the
+// cut tiles pay for their parts and the merge).
+struct AttnPlan {
+  int per, workers;
+  size_t ws_bytes;   // parts of cut tiles; 0 when tiles stay whole
+};
 
-static size_t part_o_bytes(int splits, int B, int n_q, int H) {
-  return ((size_t)splits * B * n_q * H * 4 + 255) / 256 * 256;
+static AttnPlan plan_attention(int B, int heads, int n_q, int n_kv, int d) {
+  constexpr int kSlots = 512;
+  const int nkt = n_kv / mfma_attn::BKV;
+  const int tiles = ceil_div(n_q, mfma_attn::BQ) * heads * B;
+  const long long units = (long long)tiles * nkt;
+  const int per = (int)((units + kSlots - 1) / kSlots);
+  const long long whole_longest = (long long)nkt * ceil_div(tiles, kSlots);
+  if (per % nkt == 0 || (long long)per * 10 >= whole_longest * 9) return {nkt, tiles, 0};
+  const int workers = (int)((units + per - 1) / per);
+  const size_t parts = (size_t)2 * workers * mfma_attn::BQ;
+  return {per, workers, (parts * d * 2 + 255) / 256 * 256 + parts * sizeof(float2)};
 }
 
 size_t attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int d, int dtype) {
-  if (n_q <= 0 || !attention_uses_mfma(d, n_kv, dtype)) return 0;
-  const int s = pick_splits(B, heads, n_q, n_kv);
-  if (s == 1) return 0;
-  return part_o_bytes(s, B, n_q, heads * d) + (size_t)s * B * heads * n_q * sizeof(float2);
+  if (n_q <= 0 || B <= 0 || heads <= 0 || !attention_uses_mfma(d, n_kv, dtype)) return 0;
+  return plan_attention(B, heads, n_q, n_kv, d).ws_bytes;
 }
 
 static bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15) == 0; }
@@ -556,7 +641,6 @@ static void launch_mfma(dim3 grid, const AttnParams& p, hipStream_t s) {
 hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
   if (p0.n_q <= 0) return hipSuccess;
   AttnParams p = p0;
-  p.splits = 1;
   // the MFMA kernel moves 16-byte chunks of Q, K and V^T (8 keys of V^T at a
   // time, all fresh or all stale)
   const bool aligned = p.fresh_begin % 8 == 0 && p.n_fresh % 8 == 0 && aligned16(p.q) &&
@@ -564,23 +648,30 @@ hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
                        (p.n_fresh == 0 || (aligned16(p.kv_fresh) && p.fresh_bs % 8 == 0 &&
                                            p.fresh_n % 8 == 0 && p.fresh_off % 8 == 0));
   if (attention_uses_mfma(p.d, p.n_kv, dtype) && aligned) {
-    const int want = pick_splits(p.B, p.heads, p.n_q, p.n_kv);
-    if (want > 1 && p.ws &&
-        p.ws_bytes >= attention_workspace_bytes(p.B, p.heads, p.n_q, p.n_kv, p.d, dtype)) {
-      p.splits = want;
-      p.part_o = reinterpret_cast<float*>(p.ws);
+    const AttnPlan plan = plan_attention(p.B, p.heads, p.n_q, p.n_kv, p.d);
+    const int nkt = p.n_kv / mfma_attn::BKV;
+    const int tiles = ceil_div(p.n_q, mfma_attn::BQ) * p.heads * p.B;
+    const bool cut = plan.ws_bytes > 0 && p.ws && p.ws_bytes >= plan.ws_bytes;
+    p.per = cut ? plan.per : nkt;
+    p.workers = cut ? plan.workers : tiles;
+    p.part_o = nullptr;
+    p.part_ml = nullptr;
+    if (cut) {
+      const size_t parts = (size_t)2 * p.workers * mfma_attn::BQ;
+      p.part_o = p.ws;
       p.part_ml = reinterpret_cast<float2*>(reinterpret_cast<char*>(p.ws) +
-                                            part_o_bytes(want, p.B, p.n_q, p.heads * p.d));
+                                            (parts * p.d * 2 + 255) / 256 * 256);
     }
-    dim3 grid(ceil_div(p.n_q, mfma_attn::BQ) * p.splits * p.heads * p.B);
     if (p.d == 64)
-      launch_mfma<64>(grid, p, s);
+      launch_mfma<64>(dim3(p.workers), p, s);
     else
-      launch_mfma<72>(grid, p, s);
-    if (p.splits > 1) {
-      const size_t H = (size_t)p.heads * p.d;
-      dim3 g2(ceil_div((int)H, 256), p.B * p.n_q);
-      hipLaunchKernelGGL(attn_combine_kernel, g2, dim3(256), 0, s, p);
+      launch_mfma<72>(dim3(p.workers), p, s);
+    if (cut) {
+      const dim3 g2(ceil_div(mfma_attn::BQ * p.d / 8, 256), tiles);
+      if (p.d == 64)
+        hipLaunchKernelGGL(attn_merge_kernel<64>, g2, dim3(256), 0, s, p);
+      else
+        hipLaunchKernelGGL(attn_merge_kernel<72>, g2, dim3(256), 0, s, p);
     }
     return hipGetLastError();
   }

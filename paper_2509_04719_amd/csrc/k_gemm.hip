@@ -165,20 +165,29 @@ struct StripEpilogue {
   static constexpr int SIT = 32 * (TN / 8) / 64;       // store chunks per lane per strip
   static constexpr int RIT = 32 * (TN / 4) / 64;       // residual chunks per lane per strip
   static constexpr bool PRE_H = EPI == kEpiResidual && FM == 1 && RIT <= 8;
+  // 8-channel bias chunks: one per store chunk, or a single one when every
+  // chunk of a lane falls on the same columns (64 a multiple of TN / 8)
+  static constexpr bool BIAS8 = EPI == kEpiStore || EPI == kEpiGelu || EPI == kEpiQkv;
+  static constexpr int NB = (64 % (TN / 8) == 0) ? 1 : SIT;
   struct Pre {
-    f32x4 b[(EPI == kEpiStore || EPI == kEpiGelu) ? SIT : 1][2];
+    f32x4 b[BIAS8 ? NB : 1][2];
+    float vb[EPI == kEpiQkv ? TN / 16 : 1];
     f32x4 h[PRE_H ? RIT : 1], g[PRE_H ? RIT : 1], rb[PRE_H ? RIT : 1];
   };
 
   __device__ __forceinline__ void prefetch(Pre& pre, int lane, int m0, int n0) const {
-    if constexpr (EPI == kEpiStore || EPI == kEpiGelu) {
+    if constexpr (BIAS8) {
       constexpr int CH = TN / 8;
 #pragma unroll
-      for (int q = 0; q < SIT; ++q) {
+      for (int q = 0; q < NB; ++q) {
         const int n = n0 + ((q * 64 + lane) % CH) * 8;
         pre.b[q][0] = *reinterpret_cast<const f32x4*>(ep.bias + n);
         pre.b[q][1] = *reinterpret_cast<const f32x4*>(ep.bias + n + 4);
       }
+    }
+    if constexpr (EPI == kEpiQkv) {
+#pragma unroll
+      for (int q = 0; q < TN / 16; ++q) pre.vb[q] = ep.bias[n0 + q * 16 + (lane >> 2)];
     }
     if constexpr (PRE_H) {
       constexpr int CH = TN / 4;
@@ -207,8 +216,8 @@ struct StripEpilogue {
       const f32x4 x0 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8);
       const f32x4 x1 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8 + 4);
       if (m < M) {
-        const f32x4 b0 = pre.b[q][0];
-        const f32x4 b1 = pre.b[q][1];
+        const f32x4 b0 = pre.b[NB == 1 ? 0 : q][0];
+        const f32x4 b1 = pre.b[NB == 1 ? 0 : q][1];
         bf16x8 o;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -256,7 +265,8 @@ struct StripEpilogue {
     }
   }
 
-  __device__ __forceinline__ void rows_qkv(const float* strip, int lane, int mr, int n0) const {
+  __device__ __forceinline__ void rows_qkv(const float* strip, int lane, int mr, int n0,
+                                           const Pre& pre) const {
     const int hd = ep.head_dim, hidden = ep.hidden, rpb = ep.rows_per_batch;
     const size_t ntot = (size_t)ep.kv_tokens;
     bf16* qb = reinterpret_cast<bf16*>(ep.q);
@@ -271,8 +281,8 @@ struct StripEpilogue {
         if (m >= M || n >= 2 * hidden) continue;
         const f32x4 x0 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8);
         const f32x4 x1 = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 8 + 4);
-        const f32x4 b0 = *reinterpret_cast<const f32x4*>(ep.bias + n);
-        const f32x4 b1 = *reinterpret_cast<const f32x4*>(ep.bias + n + 4);
+        const f32x4 b0 = pre.b[NB == 1 ? 0 : q][0];
+        const f32x4 b1 = pre.b[NB == 1 ? 0 : q][1];
         const int b = branch_of(m), tok = m - b * rpb;
         const int which = n >= hidden, nn = n - which * hidden;
         const int head = (int)__umulhi((unsigned)nn, ep.hd_magic), dd = nn - head * hd;
@@ -299,7 +309,7 @@ struct StripEpilogue {
         float v[8];
 #pragma unroll
         for (int t = 0; t < 8; ++t) v[t] = strip[(grp * 8 + t) * LS + col];
-        const float bias = ep.bias[n];
+        const float bias = pre.vb[q];
         const int nn = n - 2 * hidden, head = (int)__umulhi((unsigned)nn, ep.hd_magic), dd = nn - head * hd;
         bf16* vt = kvb + ntot * hidden + ((size_t)head * hd + dd) * ntot + ep.tok_offset;
         const int m = mr + grp * 8;
@@ -338,7 +348,7 @@ struct StripEpilogue {
               f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
       if constexpr (EPI == kEpiStore || EPI == kEpiGelu) rows_store(strip, lane, m0 + 32 * i, n0, pre);
       else if constexpr (EPI == kEpiResidual) rows_residual(strip, lane, m0 + 32 * i, n0, pre);
-      else rows_qkv(strip, lane, m0 + 32 * i, n0);
+      else rows_qkv(strip, lane, m0 + 32 * i, n0, pre);
     }
   }
 };

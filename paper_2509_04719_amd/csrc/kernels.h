@@ -52,17 +52,22 @@ struct AttnParams {
   int fresh_n, fresh_off;
   int B, heads, n_q, n_kv, d;
   void* out;                  // T [B][n_q][heads*d]
-  // split-KV workspace (optional): fp32 partials, see attention_workspace_bytes
+  // workspace (optional) for query tiles cut between workgroups, see
+  // attention_workspace_bytes
   void* ws;
   size_t ws_bytes;
-  // set by the launcher: number of key splits and, per split, the partial
-  // outputs O_s fp32 [splits][B*n_q][H] and (max, sum) float2 [splits][B][heads][n_q]
-  int splits;
-  float* part_o;
+  // set by the launcher: workgroup w takes work units [w * per, (w+1) * per)
+  // of (branch, head, 128-query tile, 64-key tile); parts of cut tiles go to
+  // part_o bf16 [2 * workers][128][d] (O_s / l_s) and part_ml float2
+  // [2 * workers][128] (max, sum), slot 2w for w's first tile, 2w + 1 for
+  // its last
+  int per, workers;
+  void* part_o;
   float2* part_ml;
 };
 
-// Workspace bytes of the split-KV path for this shape (0: no split is used).
+// Workspace bytes that let the attention cut query tiles between workgroups
+// for this shape (0: tiles stay whole).
 size_t attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int d, int dtype);
 hipError_t launch_attention(const AttnParams& p, int dtype, hipStream_t stream);
 bool attention_uses_mfma(int d, int n_kv, int dtype);

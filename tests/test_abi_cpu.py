@@ -118,3 +118,21 @@ def test_library_plan_rejects_bad_arguments(orch_lib, args, word):
     with pytest.raises(orch_lib.OrchError) as e:
         orch_lib.plan_devices(*args)
     assert e.value.code == orch_lib.ORCH_EINVAL and word in orch_lib.last_error()
+
+
+@pytest.mark.parametrize("n_q,n_kv,d,want", [
+    # DiT-XL/2 1024px, 40% band: 416 query tiles of 64 key tiles on 512
+    # workgroups -> 52 units each, every tile cut: 2 * 512 * 128 parts of
+    # 72 bf16 + (max, sum)
+    (1664, 4096, 72, 2 * 512 * 128 * (72 * 2 + 8)),
+    (2048, 4096, 72, 0),          # 512 tiles: one whole tile per workgroup
+    (4096, 4096, 72, 0),          # 1024 tiles: two whole tiles per workgroup
+    (1664, 4096, 80, 0),          # no MFMA path for d = 80
+    (1664, 4100, 72, 0),          # keys not a multiple of 64
+    (1920, 4096, 72, 0),          # 480 tiles: cutting saves under 10%
+])
+def test_attention_work_plan_workspace(orch_lib, n_q, n_kv, d, want):
+    """Host-side work plan of the attention: when query tiles are cut between
+    workgroups, and the workspace their parts take."""
+    assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, d, 1) == want
+    assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, d, 0) == 0   # fp32: no MFMA path

@@ -141,6 +141,33 @@ def test_qkv_scatter(orch_lib, dtype, H, heads, n_tok, kv_tokens, off):
         np.testing.assert_array_equal(kvh[b, 2 * kv_tokens * H:], can[b, 2 * kv_tokens * H:])
 
 
+# ---- every MFMA tile configuration ------------------------------------------
+
+N_TILES = 4     # MFMA tile configurations of the projection GEMM, fallback last
+
+
+@pytest.fixture
+def force_tile(monkeypatch):
+    def set_tile(t):
+        monkeypatch.setenv("ORCH_GEMM_TILE", str(t))
+    return set_tile
+
+
+@pytest.mark.parametrize("tile", range(N_TILES))
+@pytest.mark.parametrize("epi", [0, 1, 2])
+def test_linear_every_tile(orch_lib, force_tile, tile, epi):
+    """Each tile shape (forced; N = 768 and K = 1152 fit all of them) on a
+    ragged M, with every epilogue."""
+    force_tile(tile)
+    test_linear(orch_lib, "bf16", 333, 1152, 768, epi)
+
+
+@pytest.mark.parametrize("tile", range(N_TILES))
+def test_qkv_scatter_every_tile(orch_lib, force_tile, tile):
+    force_tile(tile)
+    test_qkv_scatter(orch_lib, "bf16", 768, 12, 200, 576, 192)
+
+
 # ---- attention over fresh + stale K/V --------------------------------------
 
 def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fresh, seed,
@@ -192,12 +219,16 @@ def test_attention(orch_lib, dtype, heads, d, n_q, n_kv, fb, nf):
 
 
 @pytest.mark.parametrize("split", [False, True])
-@pytest.mark.parametrize("n_q,n_kv,fb,nf", [(384, 4096, 1920, 384), (96, 1024, 512, 96),
-                                            (384, 1024, 0, 0)])
-def test_attention_split_keys(orch_lib, split, n_q, n_kv, fb, nf):
-    """Short bands split the keys over more workgroups (partials + combine)."""
-    assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, 72, 1) > 0
-    err = _attention_case(orch_lib, "bf16", 2, 16, 72, n_q, n_kv, fb, nf, seed=n_q + 1, split=split)
+@pytest.mark.parametrize("d,n_q,n_kv,fb,nf", [
+    (72, 384, 4096, 1920, 384), (72, 96, 1024, 512, 96), (72, 384, 1024, 0, 0),
+    (72, 200, 1024, 64, 200), (64, 1664, 2304, 256, 1664), (72, 3328, 4096, 2048, 2048)])
+def test_attention_split_keys(orch_lib, split, d, n_q, n_kv, fb, nf):
+    """With a workspace, query tiles are cut between workgroups (parts of a
+    tile from 1 to 8 workgroups, merged by a second kernel); without one,
+    every tile stays whole.  Both agree with the oracle."""
+    assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, d, 1) > 0
+    err = _attention_case(orch_lib, "bf16", 2, 16, d, n_q, n_kv, fb, nf, seed=n_q + d + 1,
+                          split=split)
     assert err <= 1e-2, err
 
 
