@@ -44,7 +44,9 @@ KERNEL_SOURCES = {
     "attention": ["paper_2509_04719_amd/csrc/k_attention.hip", "paper_2509_04719_amd/csrc/common.h",
                   "paper_2509_04719_amd/csrc/kernels.h", "paper_2509_04719_amd/build.py"],
 }
-KERNEL_NAMES = {"attention": "attn_bf16_mfma_kernel"}
+# the attention launch: the main kernel, and the merge of the query tiles it
+# cut between workgroups (absent when every tile stays whole)
+KERNEL_NAMES = {"attention": ["attn_bf16_mfma_kernel", "attn_merge_kernel"]}
 # calibration: the scheduler-update kernel with no unconditional branch and no
 # noise reads x and eps and writes out, 4 bytes each per element
 CALIB_ELEMS = 64 << 20
@@ -122,7 +124,7 @@ def pmc_report(fetch_dir: str, write_dir: str, kernel: str = "attention") -> int
             for r in csv.DictReader(open(f)):
                 if r["Counter_Name"] != counter:
                     continue
-                for key in (CALIB_NAME, KERNEL_NAMES[kernel]):
+                for key in [CALIB_NAME] + KERNEL_NAMES[kernel]:
                     if key in r["Kernel_Name"]:
                         g, v = vals.setdefault(key, {}).get(r["Dispatch_Id"], (int(r["Grid_Size"]), 0.0))
                         vals[key][r["Dispatch_Id"]] = (g, v + float(r["Counter_Value"]))
@@ -139,9 +141,9 @@ def pmc_report(fetch_dir: str, write_dir: str, kernel: str = "attention") -> int
     calib_read_kib, calib_write_kib = 8 * CALIB_ELEMS / 1024, 4 * CALIB_ELEMS / 1024
     fscale = calib_read_kib / med(fetch[CALIB_NAME])
     wscale = calib_write_kib / med(write[CALIB_NAME])
-    k = KERNEL_NAMES[kernel]
-    fb = med(fetch[k]) * fscale * 1024
-    wb = med(write[k]) * wscale * 1024
+    names = [k for k in KERNEL_NAMES[kernel] if k in fetch and k in write]
+    fb = sum(med(fetch[k]) for k in names) * fscale * 1024
+    wb = sum(med(write[k]) for k in names) * wscale * 1024
     print(f"# HBM traffic of the {kernel} kernel, DiT-XL/2 1024px band step (26 of 64 rows)\n")
     print("Commands (repository root, on the GPU host):\n")
     print("    rocprofv3 --pmc FETCH_SIZE -d <fetch_dir> -o pmc --output-format csv -- python3 bench.py --pmc-probe")
@@ -151,8 +153,10 @@ def pmc_report(fetch_dir: str, write_dir: str, kernel: str = "attention") -> int
           f"{4 * CALIB_ELEMS} B; the counters read {med(fetch[CALIB_NAME]):.1f} KiB and "
           f"{med(write[CALIB_NAME]):.1f} KiB per dispatch, so FETCH_SIZE is scaled by {fscale:.4f} and "
           f"WRITE_SIZE by {wscale:.4f}.\n")
-    print(f"Per {kernel} dispatch (median of {len(fetch[k])} / {len(write[k])}): FETCH_SIZE "
-          f"{med(fetch[k]):.1f} KiB, WRITE_SIZE {med(write[k]):.1f} KiB.\n")
+    for k in names:
+        print(f"Per `{k}` dispatch (median of {len(fetch[k])} / {len(write[k])}): FETCH_SIZE "
+              f"{med(fetch[k]):.1f} KiB, WRITE_SIZE {med(write[k]):.1f} KiB.\n")
+    print(f"A launch of the {kernel} is one dispatch of each; its bytes are their sum.\n")
     print(f"- kernel: {kernel}")
     print(f"- source_sha256: {kernel_source_hash(kernel)}")
     print(f"- fetch_bytes_per_launch: {fb:.0f}")

@@ -323,14 +323,19 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     if constexpr (!G::ONES) l_run = l_run * alpha + psum;
   };
 
-  // segments: key tiles [a, bnd) of query tile `tile`, in unit order
-  // (the divisions run on the VALU; readfirstlane keeps the segment's
-  // indices, and the loop control built on them, in SGPRs)
-  for (int u = u_begin; u < u_end;) {
-    const int tile = __builtin_amdgcn_readfirstlane(u / nkt), a = u - tile * nkt;
-    const int bnd = min(nkt, a + (u_end - u));
-    const bool first = u == u_begin;
-    u += bnd - a;
+  // segments: key tiles [a, bnd) of query tile `tile`, last tile of the
+  // range first.  With at most two segments (a range shorter than a tile),
+  // every workgroup then starts at key tile 0 and, in its second segment,
+  // reads key tile tau + nkt - per at time tau: the workgroups of one head
+  // sweep its K/V in step and share each tile in L2.  (The divisions run on
+  // the VALU; readfirstlane keeps the segment's indices, and the loop
+  // control built on them, in SGPRs.)
+  const int tile_first = __builtin_amdgcn_readfirstlane(u_begin / nkt);
+  for (int ue = u_end; ue > u_begin;) {
+    const int tile = __builtin_amdgcn_readfirstlane((ue - 1) / nkt);
+    const int a = max(u_begin - tile * nkt, 0), bnd = ue - tile * nkt;
+    const bool first = ue == u_end;                 // first segment processed
+    ue = tile * nkt + a;
     const int pair = __builtin_amdgcn_readfirstlane(tile / n_qt), qt = tile - pair * n_qt;
     const int b = __builtin_amdgcn_readfirstlane(pair / p.heads), head = pair - b * p.heads;
     const int q0 = qt * BQ, kv0 = a * BKV, NIT = bnd - a;
@@ -431,11 +436,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
       l = l_run + __shfl_xor(l_run, 32, kWave);
     }
     // a whole query tile goes to the output; the part of a cut one to this
-    // workgroup's slot (2w: its first segment, 2w + 1: its last) as O_s / l_s
-    // in bf16 with (max, sum), for the merge
+    // workgroup's slot (2w: the first tile of its range, 2w + 1: the last) as
+    // O_s / l_s in bf16 with (max, sum), for the merge
     const int ql = wave * 32 + lc, q = q0 + ql;
     const bool whole = a == 0 && bnd == nkt;
-    const int slot = 2 * w + (first ? 0 : 1);
+    const int slot = 2 * w + (tile == tile_first ? 0 : 1);
     const float inv = 1.0f / l;
     if (q < p.n_q) {
       bf16* orow = whole ? reinterpret_cast<bf16*>(p.out) + ((size_t)b * p.n_q + q) * H + head * D
