@@ -283,6 +283,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
         for (int e = 0; e < 8; ++e) pp[ci][e] = (bf16)((float)pp[ci][e] * alpha);
     }
     __builtin_amdgcn_sched_barrier(0);
+    // the MFMA-dense part runs at raised wave priority: the two waves sharing a
+    // SIMD then fall out of step, one in its softmax while the other issues
+    // MFMAs (measured 3-4% faster than equal priorities)
+    __builtin_amdgcn_s_setprio(1);
     if constexpr (NEXT) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) sn[r] = 0.0f;
@@ -320,6 +324,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
       // the MFMAs, instead of sunk into the next block
       asm volatile("" ::"v"(pc[ci]));
     });
+    __builtin_amdgcn_s_setprio(0);
     if constexpr (!G::ONES) l_run = l_run * alpha + psum;
   };
 
