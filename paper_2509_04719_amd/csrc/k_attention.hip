@@ -214,9 +214,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   // fragment read offsets: K row sub*32 + lc, logical chunk 2c + h; V^T row
   // t*32 + lc, logical chunk 2c + h (the swizzle depends on lc only).  V^T
   // rows >= D are the shared constant rows.
-  int k_rd[NC];
+  // (unswizzled rows: one base, the chunks at immediate offsets 32 c)
+  int k_rd[G::KSWZ ? NC : 1];
 #pragma unroll
-  for (int c = 0; c < NC; ++c)
+  for (int c = 0; c < (G::KSWZ ? NC : 1); ++c)
     k_rd[c] = lc * G::KROW + (G::KSWZ ? ((2 * c + h) ^ ((lc >> 1) & 7)) : (2 * c + h)) * 16;
   int v_rd[4];
 #pragma unroll
@@ -225,13 +226,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
 
   const float scale = 1.4426950408889634f / sqrtf((float)D);  // log2(e) / sqrt(d)
   float m_run, l_run;
-  f32x16 o[NT];
+  f32x16 o[NT], negm;   // negm: -m_run in every element, the input of each score chain
 
   // K fragments of half `sub` (keys [32 sub, +32)) of the tile in stage st
   auto k_frags = [&](int st, int sub, bf16x8(&kf_)[NC]) {
     const char* sk = smem + st * G::STAGE + sub * 32 * G::KROW;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) kf_[c] = *reinterpret_cast<const bf16x8*>(sk + k_rd[c]);
+    for (int c = 0; c < NC; ++c)
+      kf_[c] = *reinterpret_cast<const bf16x8*>(sk + (G::KSWZ ? k_rd[c] : k_rd[0] + 32 * c));
   };
   // V^T fragment of O^T tile tt and 16-key chunk c of the tile in stage st
   auto v_frag = [&](int st, int tt, int c) {
@@ -247,16 +249,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   // nsub, into sn) and of the previous half's O^T += V^T P^T (probabilities
   // pp, V^T of stage pst, half psub), so a wave keeps its matrix core busy
   // through the softmax.  This half's probabilities go to pc.
-  auto step = [&](auto next_c, int st, int sub, const f32x16& sc, int nst, int nsub, f32x16& sn,
-                  int pst, int psub, bf16x8(&pp)[2], bf16x8(&pc)[2]) {
+  auto step = [&](auto next_c, bool start, int st, int sub, f32x16& sc, int nst, int nsub,
+                  f32x16& sn, int pst, int psub, bf16x8(&pp)[2], bf16x8(&pc)[2]) {
     constexpr bool NEXT = decltype(next_c)::value;
-    // online softmax over this lane's query column.  The running max is a
-    // whole number, raised only when some lane's max exceeds it by more than
-    // 8 (log2 units): until then exp2(s - m_run) <= 2^8, exact in fp32 and in
-    // range for bf16, so O is rarely rescaled; when it is, by a power of two,
-    // which scales the previous half's pending probabilities exactly too.
-    // the fragment reads go first, in order of use; the max below covers
-    // their latency
+    // online softmax over this lane's query column.  Q carries log2(e)/sqrt(d)
+    // and every score chain starts from -m_run (the accumulator input), so sc
+    // holds s - m_run and the probability is exp2(sc) with nothing in between.
+    // The running max m_run is a whole number, set on a segment's first half
+    // and raised only when some lane's max exceeds it by more than 8: until
+    // then exp2(sc) <= 2^8, exact in fp32 and in range for bf16, so O is
+    // rarely rescaled; when it is, by a power of two, which scales the
+    // previous half's pending probabilities exactly too.  The fragment reads
+    // go first, in order of use; the max below covers their latency.
     bf16x8 vp[2][NT];
 #pragma unroll
     for (int ci = 0; ci < 2; ++ci)
@@ -267,12 +271,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     float mx = fmaxf(sc[0], sc[1]);
 #pragma unroll
     for (int r = 2; r < 16; r += 2) mx = fmaxf(mx, fmaxf(sc[r], sc[r + 1]));
-    mx = max_xhalf(mx) * scale;   // VALU swap: no LDS round trip behind the fragment reads
+    mx = max_xhalf(mx);   // VALU swap: no LDS round trip behind the fragment reads
     float alpha = 1.0f;
-    if (__builtin_expect(__any(mx > m_run + 8.0f), 0)) {
-      const float m_new = fmaxf(m_run, ceilf(mx));
-      alpha = ldexpf(1.0f, (int)fmaxf(m_run - m_new, -160.0f));
-      m_run = m_new;
+    if (__builtin_expect(__any(start || mx > 8.0f), 0)) {
+      // raise (or, on a segment's first half, set) the max by a whole d
+      const float d = (start || mx > 8.0f) ? ceilf(mx) : 0.0f;
+      alpha = start ? 1.0f : ldexpf(1.0f, -(int)fminf(d, 160.0f));
+      m_run += d;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sc[r] -= d;
+        negm[r] = -m_run;
+      }
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
@@ -287,10 +297,6 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     // SIMD then fall out of step, one in its softmax while the other issues
     // MFMAs (measured 3-4% faster than equal priorities)
     __builtin_amdgcn_s_setprio(1);
-    if constexpr (NEXT) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sn[r] = 0.0f;
-    }
     float psum = 0.0f;
     // per 16-key chunk ci: NM MFMAs (PV and S alternating, PV first) in
     // groups, each followed by its share of the chunk's 4 pairs of
@@ -306,13 +312,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
         if constexpr (pv)
           o[idx] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[ci][idx], pp[ci], o[idx], 0, 0, 0);
         else
-          sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c0 + idx], qf[c0 + idx], sn, 0, 0, 0);
+          sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c0 + idx], qf[c0 + idx],
+                                                      c0 + idx == 0 ? negm : sn, 0, 0, 0);
         static_for<g * 4 / NM, (g + 1) * 4 / NM>([&](auto pc_) {
           constexpr int pr = decltype(pc_)::value;
 #pragma unroll
           for (int e = 2 * pr; e < 2 * pr + 2; ++e) {
             const int r = 4 * (2 * ci + (e >> 2)) + (e & 3);
-            const float pv_ = __builtin_amdgcn_exp2f(fmaf(sc[r], scale, -m_run));
+            const float pv_ = __builtin_amdgcn_exp2f(sc[r]);
             if constexpr (!G::ONES) psum += pv_;
             pc[ci][e] = (bf16)pv_;
           }
@@ -366,13 +373,21 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     for (int c = 0; c < NC; ++c) {
       const int d0 = c * 16 + h * 8;
       if (d0 < D) {
-        qf[c] = *reinterpret_cast<const bf16x8*>(qbase + (size_t)qrow * D + d0);
+        const bf16x8 qv = *reinterpret_cast<const bf16x8*>(qbase + (size_t)qrow * D + d0);
+        if (p.q_scaled) {
+          qf[c] = qv;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)((float)qv[e] * scale);
+        }
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)0.0f;
       }
     }
-    m_run = -1e30f;
+    m_run = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) negm[r] = 0.0f;
     l_run = 0.0f;
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
@@ -389,10 +404,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     f32x16 s0, s1;
     bf16x8 kn[NC];
     k_frags(0, 0, kn);   // the first half's scores
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[0], qf[0], negm, 0, 0, 0);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s0[r] = 0.0f;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], s0, 0, 0, 0);
+    for (int c = 1; c < NC; ++c) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], s0, 0, 0, 0);
 
     // probabilities of the previous and the current half, ping-pong; the
     // first half's "previous" is zero against resident V^T rows
@@ -405,18 +419,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     for (; t + 1 < NIT; ++t) {
       const int st = t % NSTAGE;
       const int pst = t == 0 ? st : (t + NSTAGE - 1) % NSTAGE;
-      step(std::true_type{}, st, 0, s0, st, 1, s1, pst, t == 0 ? 0 : 1, pa, pb);
+      step(std::true_type{}, t == 0, st, 0, s0, st, 1, s1, pst, t == 0 ? 0 : 1, pa, pb);
       // tile t+1 resident; stage (t-1) % NSTAGE is free for tile t+3
       wait_tiles(t + 2 < NIT ? 1 : 0);
       lds_barrier();
       if (t + NSTAGE - 1 < NIT) issue(kv0 + (t + NSTAGE - 1) * BKV, (t + NSTAGE - 1) % NSTAGE);
-      step(std::true_type{}, st, 1, s1, (t + 1) % NSTAGE, 0, s0, st, 0, pb, pa);
+      step(std::true_type{}, false, st, 1, s1, (t + 1) % NSTAGE, 0, s0, st, 0, pb, pa);
     }
     {
       const int st = t % NSTAGE;
       const int pst = t == 0 ? st : (t + NSTAGE - 1) % NSTAGE;
-      step(std::true_type{}, st, 0, s0, st, 1, s1, pst, t == 0 ? 0 : 1, pa, pb);
-      step(std::false_type{}, st, 1, s1, 0, 0, s0, st, 0, pb, pa);
+      step(std::true_type{}, t == 0, st, 0, s0, st, 1, s1, pst, t == 0 ? 0 : 1, pa, pb);
+      step(std::false_type{}, false, st, 1, s1, 0, 0, s0, st, 0, pb, pa);
       // the last half's PV
       bf16x8 vp[2][NT];
 #pragma unroll
@@ -552,8 +566,9 @@ __global__ __launch_bounds__(64) void attn_simt_kernel(AttnParams p) {
     vf = reinterpret_cast<const T*>(p.kv_fresh) + b * p.fresh_bs + (size_t)p.fresh_n * H +
          (size_t)head * D * p.fresh_n + p.fresh_off;
   }
+  // scores in the log2 domain: q carries log2(e)/sqrt(d) when p.q_scaled
   float qr[D], acc[D];
-  const float scale = 1.0f / sqrtf((float)D);
+  const float scale = p.q_scaled ? 1.0f : 1.4426950408889634f / sqrtf((float)D);
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     qr[d] = to_f<T>(qv[d]) * scale;
@@ -568,8 +583,8 @@ __global__ __launch_bounds__(64) void attn_simt_kernel(AttnParams p) {
 #pragma unroll
     for (int d = 0; d < D; ++d) s = fmaf(qr[d], to_f<T>(kr[d]), s);
     const float mn = fmaxf(m, s);
-    const float a = expf(m - mn);
-    const float e = expf(s - mn);
+    const float a = exp2f(m - mn);
+    const float e = exp2f(s - mn);
     l = l * a + e;
 #pragma unroll
     for (int d = 0; d < D; ++d) {

@@ -25,10 +25,11 @@ struct Epilogue {
   struct Col {
     bool on;
     float bias;
-    // QKV: destination of (branch 0, token 0) and strides
+    // QKV: destination of (branch 0, token 0), strides, factor (Q: q_scale)
     T* base;
     size_t bstride;
     int tstride;
+    float mul = 1.0f;
     // RESIDUAL: gate pointer of branch 0
     const float* gate;
   };
@@ -52,6 +53,7 @@ struct Epilogue {
       const int dd = nn - head * ep.head_dim;
       const size_t ntot = (size_t)ep.kv_tokens;
       if (which == 0) {
+        c.mul = ep.q_scale;
         c.base = reinterpret_cast<T*>(ep.q) + (size_t)head * ep.rows_per_batch * ep.head_dim + dd;
         c.bstride = (size_t)ep.heads * ep.rows_per_batch * ep.head_dim;
         c.tstride = ep.head_dim;
@@ -96,11 +98,11 @@ struct Epilogue {
         if (sizeof(T) == 2 && c.tstride == 1 && ((uintptr_t)dst & 7) == 0) {
           bf16x4 w;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) w[r] = (bf16)(v[r] + c.bias);
+          for (int r = 0; r < 4; ++r) w[r] = (bf16)((v[r] + c.bias) * c.mul);
           *reinterpret_cast<bf16x4*>(dst) = w;
         } else {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) dst[(size_t)r * c.tstride] = from_f<T>(v[r] + c.bias);
+          for (int r = 0; r < 4; ++r) dst[(size_t)r * c.tstride] = from_f<T>((v[r] + c.bias) * c.mul);
         }
       } else {
         for (int r = 0; r < 4; ++r) {
@@ -108,7 +110,7 @@ struct Epilogue {
           if (mm >= M) break;
           const int bb = branch_of(mm);
           const int tk = mm - bb * ep.rows_per_batch;
-          c.base[bb * c.bstride + (size_t)tk * c.tstride] = from_f<T>(v[r] + c.bias);
+          c.base[bb * c.bstride + (size_t)tk * c.tstride] = from_f<T>((v[r] + c.bias) * c.mul);
         }
       }
     }
@@ -285,14 +287,15 @@ struct StripEpilogue {
         const f32x4 b1 = pre.b[NB == 1 ? 0 : q][1];
         const int b = branch_of(m), tok = m - b * rpb;
         const int which = n >= hidden, nn = n - which * hidden;
+        const float mul = which ? 1.0f : ep.q_scale;
         const int head = (int)__umulhi((unsigned)nn, ep.hd_magic), dd = nn - head * hd;
         bf16* dst = which == 0 ? qb + (((size_t)b * ep.heads + head) * rpb + tok) * hd + dd
                                : kvb + b * ep.kv_branch_stride + ((size_t)head * ntot + ep.tok_offset + tok) * hd + dd;
         bf16x8 o;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          o[r] = from_f<bf16>(x0[r] + b0[r]);
-          o[4 + r] = from_f<bf16>(x1[r] + b1[r]);
+          o[r] = from_f<bf16>((x0[r] + b0[r]) * mul);
+          o[4 + r] = from_f<bf16>((x1[r] + b1[r]) * mul);
         }
         *reinterpret_cast<bf16x8*>(dst) = o;
       }

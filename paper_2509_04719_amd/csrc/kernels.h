@@ -25,6 +25,7 @@ struct EpiParams {
   int tok_offset;             // destination token of the first row
   int heads, hidden, head_dim;
   unsigned hd_magic;          // set by the launcher: ceil(2^32 / head_dim)
+  float q_scale = 1.0f;       // Q is written as (acc + bias) * q_scale, then rounded
 };
 
 // y = A W^T (+ epilogue).  A T [M][K], W T [N][K].
@@ -64,6 +65,9 @@ struct AttnParams {
   int per, workers;
   void* part_o;
   float2* part_ml;
+  // 1: q already carries log2(e)/sqrt(d) (the step's QKV epilogue applies it
+  // before rounding); 0: the kernels apply it
+  int q_scaled = 0;
 };
 
 // Workspace bytes that let the attention cut query tiles between workgroups

@@ -562,7 +562,11 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
       HIP_TRY(launch_layernorm_modulate(x->h, M, H, n_tok, mb, mb + H, x->n_mod, x->u, dt, s), "LN1 launch");
     }
 
+    // with the MFMA attention, Q leaves the QKV epilogue already multiplied
+    // by log2(e)/sqrt(d) (before its one rounding to bf16)
+    const bool q_scaled = dt == kBF16 && attention_uses_mfma(x->d, x->n_kv, dt);
     EpiParams eq{};
+    eq.q_scale = q_scaled ? 1.4426950408889634f / sqrtf((float)x->d) : 1.0f;
     eq.bias = x->b_qkv[l];
     eq.rows_per_batch = n_tok;
     eq.q = x->q;
@@ -590,6 +594,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
       ap.n_fresh = n_tok; ap.fresh_n = n_tok; ap.fresh_off = 0;
     }
     ap.B = B; ap.heads = x->heads; ap.n_q = n_tok; ap.n_kv = x->n_kv; ap.d = x->d; ap.out = x->att;
+    ap.q_scaled = q_scaled;
     ap.ws = x->attn_ws; ap.ws_bytes = x->attn_ws_bytes;
     {
       KernelTimer kt(x, ORCH_KCLASS_ATTENTION, s);
