@@ -204,10 +204,19 @@ enum { ORCH_EPI_STORE = 0, ORCH_EPI_GELU = 1, ORCH_EPI_RESIDUAL = 2 };
 /* y = A W^T + bias with A T [M][K], W T [N][K], bias fp32 [N], fp32
  * accumulation.  epilogue STORE: out T [M][N] = y.  GELU: out T = GELU_tanh(y).
  * RESIDUAL: out fp32 [M][N] += gate[b][n] * y, gate fp32 rows of a
- * [B][gate_stride] array, b = m / rows_per_batch. */
+ * [B][gate_stride] array, b = m / rows_per_batch.
+ * workspace: device memory of at least orch_linear_workspace_bytes() bytes
+ * (16-byte aligned) lets a GEMM with too few output tiles to fill the GPU
+ * split K over more workgroups (fp32 partials, then a reduction that applies
+ * the epilogue); NULL (or fewer bytes) runs unsplit.  The result does not
+ * depend on the split beyond rounding. */
 int orch_op_linear(const void* A, int M, int K, const void* W, int N, const float* bias,
                    int epilogue, const float* gate, int gate_stride, int rows_per_batch,
-                   void* out, int dtype, void* hip_stream);
+                   void* out, void* workspace, size_t workspace_bytes, int dtype,
+                   void* hip_stream);
+
+/* Workspace bytes orch_op_linear can use for this shape (0: never splits). */
+size_t orch_linear_workspace_bytes(int M, int N, int K, int dtype);
 
 /* The QKV projection with its scatter epilogue.  A T [B*n_tok][K], W T
  * [3H][K], bias fp32 [3H].  Q goes to q_out T [B][heads][n_tok][d]; K and V

@@ -24,6 +24,7 @@ SYMBOLS = (
     "orch_last_error", "orch_op_layernorm_modulate", "orch_op_linear", "orch_op_qkv_projection",
     "orch_op_attention", "orch_op_conditioning", "orch_op_patch_embed", "orch_op_final_layer",
     "orch_attention_workspace_bytes", "orch_set_kernel_timing", "orch_kernel_times",
+    "orch_linear_workspace_bytes",
     "orch_plan_devices", "orch_sample_patch_parallel",
 )
 KCLASSES = ("conditioning", "patch_embed", "layernorm", "qkv_gemm", "attention", "proj_gemm",
@@ -68,7 +69,8 @@ def _load():
         "orch_schedule_coefficients": (i, [C.POINTER(OrchConfig), i, i, d, C.POINTER(d)]),
         "orch_last_error": (C.c_char_p, []),
         "orch_op_layernorm_modulate": (i, [vp, i, i, i, vp, vp, i, vp, i, vp]),
-        "orch_op_linear": (i, [vp, i, i, vp, i, vp, i, vp, i, i, vp, i, vp]),
+        "orch_op_linear": (i, [vp, i, i, vp, i, vp, i, vp, i, i, vp, vp, sz, i, vp]),
+        "orch_linear_workspace_bytes": (sz, [i, i, i, i]),
         "orch_op_qkv_projection": (i, [vp, i, i, i, vp, vp, i, i, vp, vp, sz, i, i, i, vp]),
         "orch_op_attention": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, vp, sz, i, vp]),
         "orch_attention_workspace_bytes": (sz, [i, i, i, i, i, i]),
@@ -213,9 +215,15 @@ def layernorm_modulate(x, rows, hidden, rows_per_batch, shift, scale, mod_stride
 
 
 def linear(A, M, K, W, N, bias, epilogue, gate, gate_stride, rows_per_batch, out, dtype,
-           stream=None):
+           stream=None, workspace=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     check(lib.orch_op_linear(_ptr(A), M, K, _ptr(W), N, _ptr(bias), epilogue, _ptr(gate),
-                             gate_stride, rows_per_batch, _ptr(out), dtype, _stream(stream)))
+                             gate_stride, rows_per_batch, _ptr(out), _ptr(workspace), ws_bytes,
+                             dtype, _stream(stream)))
+
+
+def linear_workspace_bytes(M, N, K, dtype) -> int:
+    return lib.orch_linear_workspace_bytes(M, N, K, dtype)
 
 
 def qkv_projection(A, B, n_tok, K, W, bias, hidden, heads, q_out, kv_out, kv_branch_stride,

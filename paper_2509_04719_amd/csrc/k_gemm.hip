@@ -144,6 +144,7 @@ struct StripEpilogue {
 
   const EpiParams& ep;
   int M, N;
+  int split;   // kEpiPartial: this workgroup's k-split
 
   __device__ __forceinline__ int branch_of(int m) const {
     int b = 0;
@@ -337,6 +338,19 @@ struct StripEpilogue {
     }
   }
 
+  // a k-split's partial sums, fp32 rows of ws[split]
+  __device__ __forceinline__ void rows_partial(const float* strip, int lane, int mr, int n0) const {
+    constexpr int CH = TN / 4, IT = 32 * CH / 64;
+    float* wb = ep.ws + (size_t)split * M * N;
+#pragma unroll
+    for (int q = 0; q < IT; ++q) {
+      const int f = q * 64 + lane, row = f / CH, c = f % CH;
+      const int m = mr + row, n = n0 + c * 4;
+      if (m < M)
+        *reinterpret_cast<f32x4*>(wb + (size_t)m * N + n) = *reinterpret_cast<const f32x4*>(strip + row * LS + c * 4);
+    }
+  }
+
   // the wave's tile: rows [m0, m0 + 32 FM), columns [n0, n0 + TN)
   __device__ __forceinline__ void run(const f32x16 (&acc)[FM][FN], float* strip, int lane, int m0,
                                       int n0, const Pre& pre) const {
@@ -351,6 +365,7 @@ struct StripEpilogue {
               f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
       if constexpr (EPI == kEpiStore || EPI == kEpiGelu) rows_store(strip, lane, m0 + 32 * i, n0, pre);
       else if constexpr (EPI == kEpiResidual) rows_residual(strip, lane, m0 + 32 * i, n0, pre);
+      else if constexpr (EPI == kEpiPartial) rows_partial(strip, lane, m0 + 32 * i, n0);
       else rows_qkv(strip, lane, m0 + 32 * i, n0, pre);
     }
   }
@@ -394,7 +409,7 @@ struct GemmGeo {
 template <int BM, int BN, int BK, int WM, int WN, int S, int EPI>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(const bf16* __restrict__ A,
                                                         const bf16* __restrict__ W, int M, int N,
-                                                        int K, int tiles_m, int tiles_n,
+                                                        int K, int ldk, int tiles_m, int tiles_n,
                                                         EpiParams ep) {
   using G = GemmGeo<BM, BN, BK, WM, WN, S>;
   constexpr int FM = G::FM, FN = G::FN, KK = G::KK, IA = G::IA, LPT = G::LPT, LPK = G::LPK;
@@ -406,9 +421,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(const bf16* __r
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
-  // tile order: XCD-major, then groups of 8 tile rows, column-major inside
-  int pid = blockIdx.x;
+  // K is this workgroup's k extent, ldk the row stride of A and W: with a
+  // k-split, workgroup b takes split b / T, keys [split K, (split + 1) K).
+  // Tile order inside a split: XCD-major, then groups of 8 tile rows,
+  // column-major inside.
   const int T = tiles_m * tiles_n;
+  const int split = __builtin_amdgcn_readfirstlane(blockIdx.x / T);
+  int pid = blockIdx.x - split * T;
   const int per = T / 8;
   if (pid < per * 8) pid = (pid & 7) * per + (pid >> 3);
   constexpr int GROUP = 8;
@@ -431,10 +450,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(const bf16* __r
     const int r = (i * G::NW + wave) * G::RPL + prow;
     const int lchunk = pchunk ^ ((r / G::Q) % G::CPR);
     const unsigned row = j < IA ? (unsigned)min(m0 + r, M - 1) : (unsigned)(n0 + r);
-    off[j] = (row * (unsigned)K + lchunk * 8) * 2u;
+    off[j] = (row * (unsigned)ldk + lchunk * 8) * 2u;
   }
-  const char* gA = reinterpret_cast<const char*>(A);
-  const char* gW = reinterpret_cast<const char*>(W);
+  const char* gA = reinterpret_cast<const char*>(A + (size_t)split * K);
+  const char* gW = reinterpret_cast<const char*>(W + (size_t)split * K);
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -506,7 +525,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(const bf16* __r
 
   // epilogue operands first: the oldest loads, covered by the main loop
   using E = StripEpilogue<FM, FN, EPI>;
-  const E epi{ep, M, N};
+  const E epi{ep, M, N, split};
   typename E::Pre pre;
   epi.prefetch(pre, lane, m0 + wm * G::TM, n0 + wn * G::TN);
 
@@ -660,7 +679,7 @@ static bool mfma_path_ok(const void* A, const void* W, int N, int K, int epi, co
 
 template <int BM, int BN, int BK, int WM, int WN, int S, int EPI>
 static void launch_tile(const void* A, const void* W, int M, int N, int K, const EpiParams& ep0,
-                        hipStream_t s) {
+                        hipStream_t s, int splits = 1) {
   const int tm = ceil_div(M, BM), tn = N / BN;
   constexpr int lds = S * GemmGeo<BM, BN, BK, WM, WN, S>::STAGE;
   EpiParams ep = ep0;
@@ -673,9 +692,51 @@ static void launch_tile(const void* A, const void* W, int M, int N, int K, const
     return true;
   }();
   (void)attr;
-  hipLaunchKernelGGL(kern, dim3(tm * tn), dim3(64 * WM * WN), lds, s,
-                     reinterpret_cast<const bf16*>(A), reinterpret_cast<const bf16*>(W), M, N, K,
-                     tm, tn, ep);
+  hipLaunchKernelGGL(kern, dim3(tm * tn * splits), dim3(64 * WM * WN), lds, s,
+                     reinterpret_cast<const bf16*>(A), reinterpret_cast<const bf16*>(W), M, N,
+                     K / splits, K, tm, tn, ep);
+}
+
+// Sum of the k-splits' partials, then the caller's epilogue (bias, GELU,
+// gated residual or the QKV scatter): four rows of one column per thread, the
+// splits added in order.
+template <typename T, int EPI>
+__global__ __launch_bounds__(256) void gemm_split_reduce_kernel(int splits, int M, int N,
+                                                                EpiParams ep) {
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  const int m = blockIdx.y * 4;
+  if (n >= N) return;
+  const Epilogue<T, EPI> epi{ep, M, N};
+  float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int sp = 0; sp < splits; ++sp) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (m + r < M) v[r] += ep.ws[((size_t)sp * M + m + r) * N + n];
+  }
+  epi.store4(epi.column(n), m, n, v);
+}
+
+// K-split of a GEMM whose tiles leave most of the machine idle (at most 128
+// tiles for 256 CUs): splits s with s * tiles <= 256, at least 8 k-tiles per
+// split, s dividing the k-tiles and the partials fitting the workspace.
+static int split_plan(int M, int N, int K, const TileCfg& t, size_t ws_elems) {
+  const int tiles = ceil_div(M, t.bm) * (N / t.bn);
+  const int kt = K / t.bk;
+  if (tiles > 128) return 1;
+  int sp = cmin(256 / tiles, kt / 8);
+  while (sp > 1 && (kt % sp != 0 || (size_t)sp * M * N > ws_elems)) --sp;
+  return sp;
+}
+
+template <int EPI>
+static void launch_tile_cfg(int c, const void* A, const void* W, int M, int N, int K,
+                            const EpiParams& ep, hipStream_t s, int splits) {
+  switch (c) {
+    case 0: launch_tile<256, 256, 64, 2, 4, 2, EPI>(A, W, M, N, K, ep, s, splits); break;
+    case 1: launch_tile<256, 192, 64, 4, 2, 2, EPI>(A, W, M, N, K, ep, s, splits); break;
+    case 2: launch_tile<128, 128, 64, 4, 2, 4, EPI>(A, W, M, N, K, ep, s, splits); break;
+    default: launch_tile<128, 64, 64, 2, 2, 2, EPI>(A, W, M, N, K, ep, s, splits); break;
+  }
 }
 
 template <int EPI>
@@ -683,11 +744,14 @@ static hipError_t launch_gemm_epi(const void* A, const void* W, int M, int N, in
                                   const EpiParams& ep, int dtype, hipStream_t s) {
   if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
   if (mfma_path_ok(A, W, N, K, EPI, ep, dtype)) {
-    switch (pick_tile(M, N, K)) {
-      case 0: launch_tile<256, 256, 64, 2, 4, 2, EPI>(A, W, M, N, K, ep, s); break;
-      case 1: launch_tile<256, 192, 64, 4, 2, 2, EPI>(A, W, M, N, K, ep, s); break;
-      case 2: launch_tile<128, 128, 64, 4, 2, 4, EPI>(A, W, M, N, K, ep, s); break;
-      default: launch_tile<128, 64, 64, 2, 2, 2, EPI>(A, W, M, N, K, ep, s); break;
+    const int c = pick_tile(M, N, K);
+    const int sp = ep.ws && aligned16(ep.ws) ? split_plan(M, N, K, kTiles[c], ep.ws_elems) : 1;
+    if (sp > 1) {
+      launch_tile_cfg<kEpiPartial>(c, A, W, M, N, K, ep, s, sp);
+      hipLaunchKernelGGL((gemm_split_reduce_kernel<bf16, EPI>), dim3(ceil_div(N, 256), ceil_div(M, 4)),
+                         dim3(256), 0, s, sp, M, N, ep);
+    } else {
+      launch_tile_cfg<EPI>(c, A, W, M, N, K, ep, s, 1);
     }
   } else {
     dim3 grid(ceil_div(N, simt_gemm::BN), ceil_div(M, simt_gemm::BM));
@@ -701,6 +765,14 @@ static hipError_t launch_gemm_epi(const void* A, const void* W, int M, int N, in
                          M, N, K, ep);
   }
   return hipGetLastError();
+}
+
+size_t gemm_split_workspace_elems(int M, int N, int K, int dtype) {
+  if (M <= 0 || !gemm_uses_mfma(N, K, dtype)) return 0;
+  const int c = pick_tile(M, N, K);
+  if (!tile_fits(kTiles[c], N, K)) return 0;
+  const int sp = split_plan(M, N, K, kTiles[c], (size_t)-1);
+  return sp > 1 ? (size_t)sp * M * N : 0;
 }
 
 hipError_t launch_gemm(const void* A, const void* W, int M, int N, int K, int epi,

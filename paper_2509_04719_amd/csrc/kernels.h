@@ -8,7 +8,9 @@
 namespace orch {
 
 enum Dtype { kF32 = 0, kBF16 = 1 };
-enum Epi { kEpiStore = 0, kEpiGelu = 1, kEpiResidual = 2, kEpiQkv = 3 };
+// kEpiPartial (internal): a k-split's fp32 partial sums, reduced by a second
+// kernel that applies the caller's epilogue
+enum Epi { kEpiStore = 0, kEpiGelu = 1, kEpiResidual = 2, kEpiQkv = 3, kEpiPartial = 4 };
 
 // Epilogue parameters of the projection GEMMs.
 struct EpiParams {
@@ -26,7 +28,14 @@ struct EpiParams {
   int heads, hidden, head_dim;
   unsigned hd_magic;          // set by the launcher: ceil(2^32 / head_dim)
   float q_scale = 1.0f;       // Q is written as (acc + bias) * q_scale, then rounded
+  // optional fp32 workspace: lets a GEMM with too few output tiles to fill
+  // the machine split K (partials [splits][M][N], then a reduction)
+  float* ws = nullptr;
+  size_t ws_elems = 0;
 };
+
+// Workspace elements (fp32) the GEMM's k-split takes for this shape (0: no split).
+size_t gemm_split_workspace_elems(int M, int N, int K, int dtype);
 
 // y = A W^T (+ epilogue).  A T [M][K], W T [N][K].
 hipError_t launch_gemm(const void* A, const void* W, int M, int N, int K, int epi,

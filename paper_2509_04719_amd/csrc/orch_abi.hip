@@ -93,6 +93,8 @@ struct orch_ctx {
   float* eps = nullptr;
   void* attn_ws = nullptr;
   size_t attn_ws_bytes = 0;
+  float* gemm_ws = nullptr;   // k-split partials of short (small-band) GEMMs
+  size_t gemm_ws_elems = 0;
   float* lat[3] = {};   // latents of the patch-parallel sampler
 
   // per-kernel timing: event pairs recorded around each launch of a step
@@ -227,7 +229,7 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
   const size_t es = esize(cfg->dtype);
   const size_t tokB = (size_t)x->B * x->n_kv;
   struct Part { size_t bytes; void** dst; };
-  void *p_h, *p_u, *p_q, *p_kvf, *p_att, *p_mlp, *p_mod, *p_t1, *p_sc, *p_eps, *p_aws;
+  void *p_h, *p_u, *p_q, *p_kvf, *p_att, *p_mlp, *p_mod, *p_t1, *p_sc, *p_eps, *p_aws, *p_gws;
   void* p_lat[3];
   const size_t lat_bytes = (size_t)cfg->in_ch * cfg->latent * cfg->latent * 4;
   // split-KV partials: the largest need over every band height
@@ -235,6 +237,17 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
   for (int r = 1; r <= x->R; ++r)
     aws = std::max(aws, attention_workspace_bytes(x->B, x->heads, r * x->R, x->n_kv, x->d, cfg->dtype));
   x->attn_ws_bytes = aws;
+  // GEMM k-split partials: the largest need over every band height and the
+  // four projections
+  size_t gws = 0;
+  for (int r = 1; r <= x->R; ++r) {
+    const int M = x->B * r * x->R;
+    gws = std::max({gws, gemm_split_workspace_elems(M, 3 * x->H, x->H, cfg->dtype),
+                    gemm_split_workspace_elems(M, x->H, x->H, cfg->dtype),
+                    gemm_split_workspace_elems(M, x->F, x->H, cfg->dtype),
+                    gemm_split_workspace_elems(M, x->H, x->F, cfg->dtype)});
+  }
+  x->gemm_ws_elems = gws;
   const Part parts[] = {
       {tokB * x->H * 4, &p_h},        {tokB * x->H * es, &p_u},
       {tokB * x->H * es, &p_q},       {2 * tokB * x->H * es, &p_kvf},
@@ -242,7 +255,8 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
       {(size_t)x->B * x->n_mod * 4, &p_mod}, {(size_t)x->H * 4, &p_t1},
       {(size_t)x->B * x->H * 4, &p_sc},
       {(size_t)x->B * cfg->out_ch * cfg->latent * cfg->latent * 4, &p_eps},
-      {aws, &p_aws}, {lat_bytes, &p_lat[0]}, {lat_bytes, &p_lat[1]}, {lat_bytes, &p_lat[2]}};
+      {aws, &p_aws}, {lat_bytes, &p_lat[0]}, {lat_bytes, &p_lat[1]}, {lat_bytes, &p_lat[2]},
+      {gws * 4, &p_gws}};
   size_t total = 0;
   for (const Part& p : parts) total += (p.bytes + 255) / 256 * 256;
   hipError_t e = hipMalloc(&x->ws, total);
@@ -258,6 +272,7 @@ int orch_create(const orch_dit_config* cfg, orch_ctx** out) {
   x->h = (float*)p_h; x->u = p_u; x->q = p_q; x->kvf = p_kvf; x->att = p_att; x->mlp = p_mlp;
   x->mod = (float*)p_mod; x->t1 = (float*)p_t1; x->sc = (float*)p_sc; x->eps = (float*)p_eps;
   x->attn_ws = aws ? p_aws : nullptr;
+  x->gemm_ws = gws ? (float*)p_gws : nullptr;
   for (int i = 0; i < 3; ++i) x->lat[i] = (float*)p_lat[i];
   *out = x;
   return ORCH_OK;
@@ -568,6 +583,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
     EpiParams eq{};
     eq.q_scale = q_scaled ? 1.4426950408889634f / sqrtf((float)x->d) : 1.0f;
     eq.bias = x->b_qkv[l];
+    eq.ws = x->gemm_ws; eq.ws_elems = x->gemm_ws_elems;
     eq.rows_per_batch = n_tok;
     eq.q = x->q;
     eq.heads = x->heads; eq.hidden = H; eq.head_dim = x->d;
@@ -604,6 +620,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
     EpiParams eo{};
     eo.out = x->h; eo.bias = x->b_proj[l]; eo.gate = mb + 2 * H; eo.gate_stride = x->n_mod;
     eo.rows_per_batch = n_tok;
+    eo.ws = x->gemm_ws; eo.ws_elems = x->gemm_ws_elems;
     {
       KernelTimer kt(x, ORCH_KCLASS_PROJ, s);
       HIP_TRY(launch_gemm(x->att, x->w_proj[l], M, H, H, kEpiResidual, eo, dt, s), "proj launch");
@@ -616,6 +633,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
 
     EpiParams e1{};
     e1.out = x->mlp; e1.bias = x->b_fc1[l];
+    e1.ws = x->gemm_ws; e1.ws_elems = x->gemm_ws_elems;
     {
       KernelTimer kt(x, ORCH_KCLASS_FC1, s);
       HIP_TRY(launch_gemm(x->u, x->w_fc1[l], M, F, H, kEpiGelu, e1, dt, s), "fc1 launch");
@@ -624,6 +642,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
     EpiParams e2{};
     e2.out = x->h; e2.bias = x->b_fc2[l]; e2.gate = mb + 5 * H; e2.gate_stride = x->n_mod;
     e2.rows_per_batch = n_tok;
+    e2.ws = x->gemm_ws; e2.ws_elems = x->gemm_ws_elems;
     {
       KernelTimer kt(x, ORCH_KCLASS_FC2, s);
       HIP_TRY(launch_gemm(x->mlp, x->w_fc2[l], M, H, F, kEpiResidual, e2, dt, s), "fc2 launch");
@@ -804,9 +823,14 @@ int orch_op_layernorm_modulate(const float* xin, int rows, int hidden, int rpb, 
   return ORCH_OK;
 }
 
+size_t orch_linear_workspace_bytes(int M, int N, int K, int dtype) {
+  if (dtype != ORCH_BF16 || M < 1 || N < 1 || K < 1) return 0;
+  return gemm_split_workspace_elems(M, N, K, dtype) * sizeof(float);
+}
+
 int orch_op_linear(const void* A, int M, int K, const void* W, int N, const float* bias,
-                   int epilogue, const float* gate, int gate_stride, int rpb, void* out, int dtype,
-                   void* hip_stream) {
+                   int epilogue, const float* gate, int gate_stride, int rpb, void* out,
+                   void* workspace, size_t workspace_bytes, int dtype, void* hip_stream) {
   if (!A || !W || !bias || !out) return fail(ORCH_EINVAL, "NULL pointer");
   if (M < 0 || K < 1 || N < 1) return fail(ORCH_EINVAL, "bad shape");
   if (dtype != ORCH_F32 && dtype != ORCH_BF16) return fail(ORCH_EINVAL, "bad dtype");
@@ -818,6 +842,10 @@ int orch_op_linear(const void* A, int M, int K, const void* W, int N, const floa
   EpiParams ep{};
   ep.out = out; ep.bias = bias; ep.gate = gate; ep.gate_stride = gate_stride;
   ep.rows_per_batch = rpb < 1 ? 1 : rpb;
+  if (workspace) {
+    ep.ws = (float*)workspace;
+    ep.ws_elems = workspace_bytes / sizeof(float);
+  }
   HIP_TRY(launch_gemm(A, W, M, N, K, epilogue, ep, dtype, (hipStream_t)hip_stream), "linear launch");
   return ORCH_OK;
 }

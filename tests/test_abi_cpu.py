@@ -136,3 +136,18 @@ def test_attention_work_plan_workspace(orch_lib, n_q, n_kv, d, want):
     workgroups, and the workspace their parts take."""
     assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, d, 1) == want
     assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, d, 0) == 0   # fp32: no MFMA path
+
+
+@pytest.mark.parametrize("M,N,K,want", [
+    # DiT-XL/2 at the 10% band (M = 768): fc2 has 54 tiles of 128x128 -> 4
+    # k-splits of 18 k-tiles, fp32 partials 4 x 768 x 1152
+    (768, 1152, 4608, 4 * 768 * 1152 * 4),
+    (768, 1152, 1152, 2 * 768 * 1152 * 4),   # out-proj: 18 k-tiles -> 2 splits of 9
+    (3328, 1152, 4608, 0),                    # 234 tiles fill the machine
+    (768, 3456, 1152, 0),                     # QKV: 162 tiles
+    (768, 1152, 4600, 0),                     # K % 64: no MFMA path
+])
+def test_linear_split_workspace(orch_lib, M, N, K, want):
+    """Host-side k-split plan of the projection GEMM."""
+    assert orch_lib.linear_workspace_bytes(M, N, K, 1) == want
+    assert orch_lib.linear_workspace_bytes(M, N, K, 0) == 0   # fp32: no MFMA path

@@ -141,6 +141,47 @@ def test_qkv_scatter(orch_lib, dtype, H, heads, n_tok, kv_tokens, off):
         np.testing.assert_array_equal(kvh[b, 2 * kv_tokens * H:], can[b, 2 * kv_tokens * H:])
 
 
+# ---- k-split of short GEMMs ---------------------------------------------------
+
+@pytest.mark.parametrize("M,K,N", [(333, 4608, 768), (768, 4608, 1152), (200, 1152, 384)])
+@pytest.mark.parametrize("epi", [0, 1, 2])
+def test_linear_split_k(orch_lib, M, K, N, epi):
+    """Few output tiles: with a workspace the GEMM splits K (fp32 partials,
+    then a reduction applying the epilogue); checked against the oracle and
+    against the unsplit launch."""
+    wsb = orch_lib.linear_workspace_bytes(M, N, K, 1)
+    assert wsb > 0
+    rng = np.random.default_rng(M + K + N + epi)
+    A = rng.standard_normal((M, K))
+    W = rng.standard_normal((N, K)) * 0.02
+    bias = rng.standard_normal(N) * 0.02
+    y = dit.linear(rounded(A, "bf16"), rounded(W, "bf16"), rounded(bias, "f32"))
+    Ad, Wd, bd = to_dev(A, "bf16"), to_dev(W, "bf16"), to_dev(bias)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    if epi == 2:
+        rpb = max(1, M // 2)
+        gate = rng.standard_normal(((M + rpb - 1) // rpb, N)) * 0.5
+        h0 = rng.standard_normal((M, N))
+        gd = to_dev(gate)
+        outs = []
+        for w in (ws, None):
+            out = to_dev(h0)
+            orch_lib.linear(Ad, M, K, Wd, N, bd, 2, gd, N, rpb, out, 1, workspace=w)
+            outs.append(to_host(out) - rounded(h0, "f32"))
+        g = rounded(gate, "f32")[np.arange(M) // rpb]
+        assert rel_l2(outs[0], g * y) <= 2e-5
+        assert rel_l2(outs[0], outs[1]) <= 2e-5
+    else:
+        outs = []
+        for w in (ws, None):
+            out = empty((M, N), "bf16")
+            orch_lib.linear(Ad, M, K, Wd, N, bd, epi, None, 0, 1, out, 1, workspace=w)
+            outs.append(to_host(out))
+        ref = dit.gelu_tanh(y) if epi == 1 else y
+        assert rel_l2(outs[0], ref) <= 5e-3
+        assert rel_l2(outs[0], outs[1]) <= 5e-3
+
+
 # ---- every MFMA tile configuration ------------------------------------------
 
 N_TILES = 4     # MFMA tile configurations of the projection GEMM, fallback last
