@@ -180,27 +180,22 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst_of(st, i), 16, o, so, 0, 0);
       }
     } else {
-      // a tile across the band edge: per-lane source (8-key groups are all
-      // fresh or all stale: fb, nf % 8 == 0); 32-bit offsets from the
-      // uniform bases keep the loop-invariant part small
+      // a tile across the band edge: each lane loads from the buffer its 8
+      // keys live in (8-key groups are all fresh or all stale: fb, nf % 8 ==
+      // 0), the two buffer loads under complementary lane masks.  A wave may
+      // then count two loads for one slot; the waits below only need at least
+      // LPW per tile, so they wait longer, never shorter.
+      const unsigned so = __builtin_amdgcn_readfirstlane((unsigned)n0 * (kwave ? 2 * D : 2));
 #pragma unroll
       for (int i = 0; i < LPW; ++i) {
-        const char* base;
-        unsigned bo;
-        if (kwave) {
-          const int e = off[i] / 2, key = e / D, col = e - key * D;
-          const int n = n0 + key;
-          const bool fr = (unsigned)(n - fb) < (unsigned)nf;
-          base = reinterpret_cast<const char*>(fr ? kf : ks);
-          bo = (unsigned)((fr ? n - fb : n) * D + col) * 2u;
+        const int n = n0 + (kwave ? (int)(off[i] / 2) / D : (int)(off[i] / 2) - vrow(i) * p.n_kv);
+        if ((unsigned)(n - fb) < (unsigned)nf) {
+          const int o = kwave ? (int)off[i] + (n0 - fb) * 2 * D
+                              : (int)off[i] - vrow(i) * (p.n_kv - fn) * 2 + (n0 - fb) * 2;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(kwave ? rkf : rvf, dst_of(st, i), 16, (unsigned)o, 0, 0, 0);
         } else {
-          const int d = vrow(i), key = off[i] / 2 - d * p.n_kv;
-          const int n = n0 + key;
-          const bool fr = (unsigned)(n - fb) < (unsigned)nf;
-          base = reinterpret_cast<const char*>(fr ? vf : vs);
-          bo = (unsigned)(fr ? d * fn + (n - fb) : d * p.n_kv + n) * 2u;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(kwave ? rks : rvs, dst_of(st, i), 16, off[i], so, 0, 0);
         }
-        __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)(base + bo), dst_of(st, i), 16, 0, 0);
       }
     }
   };
