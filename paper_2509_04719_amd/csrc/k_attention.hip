@@ -27,7 +27,11 @@
 namespace orch {
 
 namespace mfma_attn {
+// BQ queries per workgroup (32 per wave), WPC workgroups per CU.  (256-query
+// workgroups, one per CU, halve the K/V loads per CU but measured no faster,
+// and slower where the query count is not a multiple of 256.)
 constexpr int BQ = 128, BKV = 64, NSTAGE = 4;
+constexpr int NW = BQ / 32, KW = NW / 2, NTHR = 64 * NW, WPC = 512 / NTHR;
 
 template <int D>
 struct Geo {
@@ -49,16 +53,16 @@ struct Geo {
   static constexpr int LDS = DUMMY_OFF + 1024;
   static constexpr int K_LOADS = K_BYTES / 1024;    // 1 KB wave-level loads
   static constexpr int V_LOADS = V_BYTES / 1024;
-  // waves 0-1 load K, waves 2-3 V^T, LPW loads each per tile; slots past the
-  // tile's loads re-read a valid chunk into the sink, so every wave counts
-  // the same number of loads
-  static constexpr int LPW = (cmax(K_LOADS, V_LOADS) + 1) / 2;
+  // the first KW waves load K, the others V^T, LPW loads each per tile;
+  // slots past the tile's loads re-read a valid chunk into the sink, so
+  // every wave counts the same number of loads
+  static constexpr int LPW = (cmax(K_LOADS, V_LOADS) + KW - 1) / KW;
   static_assert(K_BYTES % 1024 == 0 && V_BYTES % 1024 == 0, "whole 1 KB loads");
   // 16 consecutive K rows at one 16-byte column must hit distinct 4-bank
   // groups: an odd number of chunks per row, or 8 chunks with the swizzle
   static_assert(KCH == 8 || KCH % 2 == 1, "K row layout");
-  static_assert(2 * LDS <= 160 * 1024, "two workgroups per CU");
-  static_assert(2 * LPW < 16, "loads in flight");
+  static_assert(WPC * LDS <= 160 * 1024, "workgroups per CU");
+  static_assert((NSTAGE - 1) * LPW < 64, "loads in flight");
 };
 
 // LDS row rho of a K tile holds key kperm(rho): bits 2 and 3 swapped.  The
@@ -86,7 +90,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 }  // namespace mfma_attn
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
+__global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfma_kernel(AttnParams p) {
   // the body uses device-only types (buffer resources); the host pass only
   // needs the launch stub
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -119,27 +123,27 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
   // constant LDS (never written by the tile loads): 16 zero bytes after the
   // K rows of every stage, read against zero Q padding by the last chunk of
   // row 63; V^T rows [D, DV): row D ones, the rest zero
-  for (int st = tid; st < NSTAGE * 4; st += 256)
+  for (int st = tid; st < NSTAGE * 4; st += NTHR)
     reinterpret_cast<uint32_t*>(smem + (st >> 2) * G::STAGE + G::K_BYTES)[st & 3] = 0u;
   {
     bf16* cpad = reinterpret_cast<bf16*>(smem + G::CONST_OFF);
-    for (int i = tid; i < (G::DV - D) * BKV; i += 256) cpad[i] = (bf16)(i < BKV ? 1.0f : 0.0f);
+    for (int i = tid; i < (G::DV - D) * BKV; i += NTHR) cpad[i] = (bf16)(i < BKV ? 1.0f : 0.0f);
   }
 
-  // This wave's share of a tile's loads.  Waves 0-1 load K: load j = wave +
-  // 2 i fills stage bytes [1024 j, +1024), lane slot s = 64 j + lane is row
-  // s / KCH, physical chunk s % KCH.  Waves 2-3 load V^T: load j = wave - 2 +
-  // 2 i fills K_SPAN + 1024 j, row s / 8, physical chunk s % 8, logical 8-key
-  // chunk = physical ^ ((row >> 1) & 7).  off: byte offset of the lane's
-  // source from the tile's first key in the stale buffer (the same for fresh
-  // K; fresh V^T rows have stride n_fresh).
-  const bool kwave = wave < 2;
-  const int wl = wave & 1;
+  // This wave's share of a tile's loads.  Waves [0, KW) load K: load j =
+  // wave + KW i fills stage bytes [1024 j, +1024), lane slot s = 64 j + lane
+  // is row s / KCH, physical chunk s % KCH.  Waves [KW, 2 KW) load V^T: load
+  // j = wave - KW + KW i fills K_SPAN + 1024 j, row s / 8, physical chunk
+  // s % 8, logical 8-key chunk = physical ^ ((row >> 1) & 7).  off: byte
+  // offset of the lane's source from the tile's first key in the stale buffer
+  // (the same for fresh K; fresh V^T rows have stride n_fresh).
+  const bool kwave = wave < KW;
+  const int wl = wave % KW;
   const int nload = kwave ? G::K_LOADS : G::V_LOADS;
   unsigned off[LPW];
 #pragma unroll
   for (int i = 0; i < LPW; ++i) {
-    const int j = min(wl + 2 * i, nload - 1);
+    const int j = min(wl + KW * i, nload - 1);
     const int sl = j * 64 + lane;
     if (kwave) {
       const int rho = sl / G::KCH, pc = sl % G::KCH;
@@ -151,9 +155,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_mfma_kernel(AttnParams p) {
     }
   }
   // V^T row of load slot i (V waves)
-  auto vrow = [&](int i) { return (min(wl + 2 * i, nload - 1) * 64 + lane) >> 3; };
+  auto vrow = [&](int i) { return (min(wl + KW * i, nload - 1) * 64 + lane) >> 3; };
   auto dst_of = [&](int st, int i) -> ORCH_LDS void* {
-    const int j = wl + 2 * i;
+    const int j = wl + KW * i;
     if (j >= nload) return (ORCH_LDS void*)(smem + G::DUMMY_OFF);
     return (ORCH_LDS void*)(smem + st * G::STAGE + (kwave ? 0 : G::K_SPAN) + j * 1024);
   };
@@ -626,7 +630,7 @@ struct AttnPlan {
 };
 
 static AttnPlan plan_attention(int B, int heads, int n_q, int n_kv, int d) {
-  constexpr int kSlots = 512;
+  constexpr int kSlots = 256 * mfma_attn::WPC;
   const int nkt = n_kv / mfma_attn::BKV;
   const int tiles = ceil_div(n_q, mfma_attn::BQ) * heads * B;
   const long long units = (long long)tiles * nkt;
@@ -655,7 +659,7 @@ static void launch_mfma(dim3 grid, const AttnParams& p, hipStream_t s) {
     return true;
   }();
   (void)attr;
-  hipLaunchKernelGGL(kern, grid, dim3(256), lds, s, p);
+  hipLaunchKernelGGL(kern, grid, dim3(mfma_attn::NTHR), lds, s, p);
 }
 
 hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
