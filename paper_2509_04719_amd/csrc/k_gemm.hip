@@ -719,6 +719,9 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(int splits, int 
 // K-split of a GEMM whose tiles leave most of the machine idle (at most 128
 // tiles for 256 CUs): splits s with s * tiles <= 256, at least 8 k-tiles per
 // split, s dividing the k-tiles and the partials fitting the workspace.
+// (Splits that take more than one round, e.g. 144 tiles in three splits, or
+// 378 in two, measured slower than no split: the partials' round trip
+// through HBM costs more than the idle CUs.)
 static int split_plan(int M, int N, int K, const TileCfg& t, size_t ws_elems) {
   const int tiles = ceil_div(M, t.bm) * (N / t.bn);
   const int kt = K / t.bk;

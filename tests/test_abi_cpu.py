@@ -143,6 +143,7 @@ def test_attention_work_plan_workspace(orch_lib, n_q, n_kv, d, want):
     # k-splits of 18 k-tiles, fp32 partials 4 x 768 x 1152
     (768, 1152, 4608, 4 * 768 * 1152 * 4),
     (768, 1152, 1152, 2 * 768 * 1152 * 4),   # out-proj: 18 k-tiles -> 2 splits of 9
+    (2048, 1152, 4608, 0),                    # 144 tiles: a split would take two rounds
     (3328, 1152, 4608, 0),                    # 234 tiles fill the machine
     (768, 3456, 1152, 0),                     # QKV: 162 tiles
     (768, 1152, 4600, 0),                     # K % 64: no MFMA path
