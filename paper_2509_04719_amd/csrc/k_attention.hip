@@ -40,11 +40,15 @@ struct Geo {
   static constexpr int DV = (D + 31) / 32 * 32;     // rows of O^T, padded to 32
   static constexpr int NT = DV / 32;
   static constexpr bool ONES = DV > D;              // padding row D of V^T holds 1.0
+  // d = 8 (mod 16): the upper half of the last 16-dim chunk is padding, where
+  // K reads the constant (1, 1, 1, 0, ...) and Q carries -m_run split in three
+  // bf16, so every score chain yields s - m_run from a zero accumulator
+  static constexpr bool MCOL = D % 16 == 8;
   static constexpr int KROW = 2 * D;                // bytes per K row in LDS
   static constexpr int KCH = KROW / 16;             // 16-byte chunks per K row
   static constexpr bool KSWZ = KCH == 8;            // 128-byte rows: XOR swizzle
   static constexpr int K_BYTES = BKV * KROW;
-  static constexpr int K_SPAN = (K_BYTES + 16 + 255) / 256 * 256;  // 16 zero bytes after K
+  static constexpr int K_SPAN = (K_BYTES + 16 + 255) / 256 * 256;  // 16 constant bytes after K
   static constexpr int VROW = 2 * BKV;              // bytes per V^T row
   static constexpr int V_BYTES = D * VROW;
   static constexpr int STAGE = K_SPAN + V_BYTES;
@@ -120,11 +124,14 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
   const int H = p.heads * D;
   const int fb = p.fresh_begin, nf = p.n_fresh;
 
-  // constant LDS (never written by the tile loads): 16 zero bytes after the
-  // K rows of every stage, read against zero Q padding by the last chunk of
-  // row 63; V^T rows [D, DV): row D ones, the rest zero
-  for (int st = tid; st < NSTAGE * 4; st += NTHR)
-    reinterpret_cast<uint32_t*>(smem + (st >> 2) * G::STAGE + G::K_BYTES)[st & 3] = 0u;
+  // constant LDS (never written by the tile loads): 16 bytes after the K
+  // rows of every stage, bf16 (1, 1, 1, 0, 0, 0, 0, 0), the K side of the
+  // max column; V^T rows [D, DV): row D ones, the rest zero
+  for (int st = tid; st < NSTAGE * 4; st += NTHR) {
+    const uint32_t one2 = 0x3F803F80u, one = 0x00003F80u;   // bf16 1.0 = 0x3F80
+    reinterpret_cast<uint32_t*>(smem + (st >> 2) * G::STAGE + G::K_BYTES)[st & 3] =
+        (st & 3) == 0 ? one2 : (st & 3) == 1 ? one : 0u;
+  }
   {
     bf16* cpad = reinterpret_cast<bf16*>(smem + G::CONST_OFF);
     for (int i = tid; i < (G::DV - D) * BKV; i += NTHR) cpad[i] = (bf16)(i < BKV ? 1.0f : 0.0f);
@@ -222,17 +229,46 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
 #pragma unroll
   for (int c = 0; c < 4; ++c) v_rd[c] = lc * G::VROW + ((2 * c + h) ^ ((lc >> 1) & 7)) * 16;
   const bool last_in_pad = (NT - 1) * 32 + lc >= D;   // row of the last O^T tile is padding
+  // the last K chunk of half sub: the max column's constant on the h = 1 lanes
+  int k_last[2];
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub)
+    k_last[sub] = G::MCOL && h ? G::K_BYTES
+                               : sub * 32 * G::KROW + (G::KSWZ ? k_rd[NC - 1] : k_rd[0] + 32 * (NC - 1));
 
   const float scale = 1.4426950408889634f / sqrtf((float)D);  // log2(e) / sqrt(d)
   float m_run, l_run;
-  f32x16 o[NT], negm;   // negm: -m_run in every element, the input of each score chain
+  f32x16 o[NT];
+  f32x16 negm;   // without the max column: -m_run in every element, the input of each score chain
+  const f32x16 zero16 = {};
+  // -m_run into the max column of Q (h = 1 lanes, last chunk): three bf16
+  // whose sum is exactly -m_run (each takes the next 8 significant bits by
+  // truncation; any fp32 splits so)
+  auto set_mcol = [&]() {
+    const float a0 = -m_run;
+    const float b0 = __uint_as_float(__float_as_uint(a0) & 0xFFFF0000u);
+    const float r0 = a0 - b0;
+    const float b1 = __uint_as_float(__float_as_uint(r0) & 0xFFFF0000u);
+    const float b2 = r0 - b1;
+    if (h) {
+      qf[NC - 1][0] = (bf16)b0;
+      qf[NC - 1][1] = (bf16)b1;
+      qf[NC - 1][2] = (bf16)b2;
+    }
+  };
+  // first accumulator input of a score chain
+  auto chain_in = [&]() -> const f32x16& {
+    if constexpr (G::MCOL) return zero16;
+    else return negm;
+  };
 
   // K fragments of half `sub` (keys [32 sub, +32)) of the tile in stage st
   auto k_frags = [&](int st, int sub, bf16x8(&kf_)[NC]) {
     const char* sk = smem + st * G::STAGE + sub * 32 * G::KROW;
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
+    for (int c = 0; c < NC - 1; ++c)
       kf_[c] = *reinterpret_cast<const bf16x8*>(sk + (G::KSWZ ? k_rd[c] : k_rd[0] + 32 * c));
+    kf_[NC - 1] = *reinterpret_cast<const bf16x8*>(smem + st * G::STAGE + (sub ? k_last[1] : k_last[0]));
   };
   // V^T fragment of O^T tile tt and 16-key chunk c of the tile in stage st
   auto v_frag = [&](int st, int tt, int c) {
@@ -252,8 +288,9 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
                   f32x16& sn, int pst, int psub, bf16x8(&pp)[2], bf16x8(&pc)[2]) {
     constexpr bool NEXT = decltype(next_c)::value;
     // online softmax over this lane's query column.  Q carries log2(e)/sqrt(d)
-    // and every score chain starts from -m_run (the accumulator input), so sc
-    // holds s - m_run and the probability is exp2(sc) with nothing in between.
+    // and every score chain subtracts m_run (through the max column, else as
+    // the accumulator input), so sc holds s - m_run and the probability is
+    // exp2(sc) with nothing in between.
     // The running max m_run is a whole number, set on a segment's first half
     // and raised only when some lane's max exceeds it by more than 8: until
     // then exp2(sc) <= 2^8, exact in fp32 and in range for bf16, so O is
@@ -267,9 +304,11 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
       for (int tt = 0; tt < NT; ++tt) vp[ci][tt] = v_frag(pst, tt, 2 * psub + ci);
     bf16x8 kn[NC];
     if constexpr (NEXT) k_frags(nst, nsub, kn);
-    float mx = fmaxf(sc[0], sc[1]);
+    // a chain of three-way maxima (v_max3_f32: two new values each)
+    float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
 #pragma unroll
-    for (int r = 2; r < 16; r += 2) mx = fmaxf(mx, fmaxf(sc[r], sc[r + 1]));
+    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
+    mx = fmaxf(mx, sc[15]);
     mx = max_xhalf(mx);   // VALU swap: no LDS round trip behind the fragment reads
     float alpha = 1.0f;
     if (__builtin_expect(__any(start || mx > 8.0f), 0)) {
@@ -278,9 +317,12 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
       alpha = start ? 1.0f : ldexpf(1.0f, -(int)fminf(d, 160.0f));
       m_run += d;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sc[r] -= d;
-        negm[r] = -m_run;
+      for (int r = 0; r < 16; ++r) sc[r] -= d;
+      if constexpr (G::MCOL) {
+        set_mcol();
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) negm[r] = -m_run;
       }
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt)
@@ -312,7 +354,7 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
           o[idx] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[ci][idx], pp[ci], o[idx], 0, 0, 0);
         else
           sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c0 + idx], qf[c0 + idx],
-                                                      c0 + idx == 0 ? negm : sn, 0, 0, 0);
+                                                      c0 + idx == 0 ? chain_in() : sn, 0, 0, 0);
         static_for<g * 4 / NM, (g + 1) * 4 / NM>([&](auto pc_) {
           constexpr int pr = decltype(pc_)::value;
 #pragma unroll
@@ -385,8 +427,10 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
       }
     }
     m_run = 0.0f;
+    if constexpr (!G::MCOL) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) negm[r] = 0.0f;
+      for (int r = 0; r < 16; ++r) negm[r] = 0.0f;
+    }
     l_run = 0.0f;
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
@@ -403,7 +447,7 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
     f32x16 s0, s1;
     bf16x8 kn[NC];
     k_frags(0, 0, kn);   // the first half's scores
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[0], qf[0], negm, 0, 0, 0);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[0], qf[0], chain_in(), 0, 0, 0);
 #pragma unroll
     for (int c = 1; c < NC; ++c) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c], qf[c], s0, 0, 0, 0);
 
