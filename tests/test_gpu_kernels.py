@@ -212,7 +212,11 @@ def test_qkv_scatter_every_tile(orch_lib, force_tile, tile):
 # ---- attention over fresh + stale K/V --------------------------------------
 
 def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fresh, seed,
-                    sample_rows=None, split=True):
+                    sample_rows=None, split=True, k_ramp=0.0, shift=0.0):
+    """k_ramp: key j's vector scaled by 1 + k_ramp j / n_kv (scores grow along
+    the key stream, so the running max moves mid-stream); shift: the first
+    channel of every head set to `shift` in Q and K (every score of a query
+    raised by the same large amount: softmax unchanged, running max large)."""
     H = heads * d
     R = int(np.sqrt(n_kv))
     hdr = {"hidden": H, "heads": heads, "grid": R}
@@ -223,6 +227,12 @@ def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fres
     Vs = rng.standard_normal((B, n_kv, H))
     Kf = rng.standard_normal((B, max(n_fresh, 1), H)) * scale
     Vf = rng.standard_normal((B, max(n_fresh, 1), H))
+    if k_ramp:
+        Ks *= (1.0 + k_ramp * np.arange(n_kv) / n_kv)[None, :, None]
+        Kf *= (1.0 + k_ramp * (fresh_begin + np.arange(Kf.shape[1])) / n_kv)[None, :, None]
+    if shift:
+        for arr in (q, Ks, Kf):
+            arr[:, :, 0::d] = shift
     qd = to_dev(np.stack([q[b].reshape(n_q, heads, d).transpose(1, 0, 2) for b in range(B)]), dtype)
     stale = np.concatenate([dit.kv_to_buffer_layout(hdr, Ks[b], Vs[b]) for b in range(B)])
     fresh = np.concatenate([dit.kv_to_buffer_layout(hdr, Kf[b], Vf[b]) for b in range(B)])
@@ -270,6 +280,22 @@ def test_attention_split_keys(orch_lib, split, d, n_q, n_kv, fb, nf):
     assert orch_lib.attention_workspace_bytes(2, 16, n_q, n_kv, d, 1) > 0
     err = _attention_case(orch_lib, "bf16", 2, 16, d, n_q, n_kv, fb, nf, seed=n_q + d + 1,
                           split=split)
+    assert err <= 1e-2, err
+
+
+@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("d,n_q,n_kv,fb,nf", [(72, 384, 1024, 256, 384), (64, 1664, 2304, 256, 1664),
+                                             (72, 1664, 4096, 0, 1664)])
+@pytest.mark.parametrize("k_ramp,shift", [(12.0, 0.0), (0.0, 48.0), (12.0, 48.0)])
+def test_attention_running_max(orch_lib, split, d, n_q, n_kv, fb, nf, k_ramp, shift):
+    """The lazy running max: scores growing along the key stream (the max is
+    raised and O rescaled mid-stream, also in the pending probabilities of
+    the lagging PV product), and a large common score offset (a running max
+    of several hundred in log2 units, beyond one bf16 in the d = 72 max
+    column).  Sampled query rows at the large shapes."""
+    rows = np.r_[np.arange(0, n_q, 37), n_q - 1] if n_q > 1000 else None
+    err = _attention_case(orch_lib, "bf16", 2, 16, d, n_q, n_kv, fb, nf, seed=n_q + d + 7, split=split,
+                          sample_rows=rows, k_ramp=k_ramp, shift=shift)
     assert err <= 1e-2, err
 
 
