@@ -200,78 +200,68 @@ __global__ __launch_bounds__(256) void temb2_kernel(const T* __restrict__ w2,
 }
 
 // mod[b][n] = W_ada[n] . sc[b] + b_ada[n] for every adaLN row of every block:
-// streams the whole adaLN weight once.  Each lane keeps its 8-element slices
-// of sc in registers; a wave takes RPW rows at a time (their loads in flight
-// together) and reduces the 2 * RPW dot products in one interleaved pass.
-template <typename T, int RPW>
+// streams the whole adaLN weight once.  One lane per row: the weight is held
+// in 64-row groups, 16-byte chunk k of the group's rows stored contiguously
+// ([group][chunk][64 rows][16 B], see adaln_group_index), so a wave's load
+// of chunk k is one contiguous KiB and no dot product crosses lanes.  sc
+// (both guidance branches) sits in LDS and is read as a broadcast.
+constexpr int kAdaGroup = 64;
+
+template <typename T>
 __global__ __launch_bounds__(256) void adaln_gemv_kernel(const T* __restrict__ w,
                                                          const float* __restrict__ bias,
                                                          const float* __restrict__ sc, int H,
                                                          int n_rows, int B,
                                                          float* __restrict__ mod) {
-  const int lane = threadIdx.x & 63;
-  const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int n_waves = gridDim.x * 4;
-  const int nck = H / 8;  // 8-element chunks per row
-  float xs[2][4][8];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int ck = lane + 64 * j;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      xs[0][j][e] = ck < nck ? sc[ck * 8 + e] : 0.0f;
-      xs[1][j][e] = (ck < nck && B > 1) ? sc[H + ck * 8 + e] : 0.0f;
-    }
+  constexpr int CH = 16 / sizeof(T);   // elements per 16-byte chunk
+  constexpr int U = 8;                 // chunks in flight per lane
+  __shared__ float4 xs[2 * 2048 / 4];  // sc[b][H], H <= 2048
+  const int nck = H / CH;
+  for (int i = threadIdx.x; i < 2 * H / 4; i += 256) {
+    const int b = i / (H / 4);
+    xs[i] = b < B ? reinterpret_cast<const float4*>(sc)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  for (int n0 = wave_id * RPW; n0 < n_rows; n0 += n_waves * RPW) {
-    float acc[RPW][2];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int group = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int n = group * kAdaGroup + lane;
+  if (group * kAdaGroup >= n_rows) return;
+  const uint4* wg = reinterpret_cast<const uint4*>(w) + (size_t)group * nck * kAdaGroup + lane;
+  float a0 = 0.0f, a1 = 0.0f;
+  for (int k0 = 0; k0 < nck; k0 += U) {
+    uint4 q[U];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) acc[r][0] = acc[r][1] = 0.0f;
+    for (int u = 0; u < U; ++u) q[u] = k0 + u < nck ? wg[(size_t)(k0 + u) * kAdaGroup] : make_uint4(0, 0, 0, 0);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int ck = lane + 64 * j;
-      if (ck < nck) {
+    for (int u = 0; u < U; ++u) {
+      const int k = k0 + u;
+      if (k < nck) {
+        float wv[CH];
+        if constexpr (sizeof(T) == 2) {
+          const unsigned wd[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
 #pragma unroll
-        for (int r = 0; r < RPW; ++r) {
-          const int n = min(n0 + r, n_rows - 1);
-          const T* wr = w + (size_t)n * H + ck * 8;
-          float wv[8];
-          if constexpr (sizeof(T) == 2) {
-            const bf16x8 q = *reinterpret_cast<const bf16x8*>(wr);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) wv[e] = (float)q[e];
-          } else {
-            const float4 q0 = *reinterpret_cast<const float4*>(wr);
-            const float4 q1 = *reinterpret_cast<const float4*>(wr + 4);
-            wv[0] = q0.x; wv[1] = q0.y; wv[2] = q0.z; wv[3] = q0.w;
-            wv[4] = q1.x; wv[5] = q1.y; wv[6] = q1.z; wv[7] = q1.w;
+          for (int e = 0; e < 4; ++e) {
+            wv[2 * e] = __uint_as_float(wd[e] << 16);
+            wv[2 * e + 1] = __uint_as_float(wd[e] & 0xFFFF0000u);
           }
+        } else {
+          wv[0] = __uint_as_float(q[u].x); wv[1] = __uint_as_float(q[u].y);
+          wv[2] = __uint_as_float(q[u].z); wv[3] = __uint_as_float(q[u].w);
+        }
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            acc[r][0] = fmaf(wv[e], xs[0][j][e], acc[r][0]);
-            acc[r][1] = fmaf(wv[e], xs[1][j][e], acc[r][1]);
-          }
+        for (int e4 = 0; e4 < CH / 4; ++e4) {
+          const float4 x0 = xs[(k * CH) / 4 + e4], x1 = xs[H / 4 + (k * CH) / 4 + e4];
+          a0 = fmaf(wv[4 * e4 + 0], x0.x, a0); a1 = fmaf(wv[4 * e4 + 0], x1.x, a1);
+          a0 = fmaf(wv[4 * e4 + 1], x0.y, a0); a1 = fmaf(wv[4 * e4 + 1], x1.y, a1);
+          a0 = fmaf(wv[4 * e4 + 2], x0.z, a0); a1 = fmaf(wv[4 * e4 + 2], x1.z, a1);
+          a0 = fmaf(wv[4 * e4 + 3], x0.w, a0); a1 = fmaf(wv[4 * e4 + 3], x1.w, a1);
         }
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1)
-#pragma unroll
-      for (int r = 0; r < RPW; ++r) {
-        acc[r][0] += __shfl_xor(acc[r][0], o, kWave);
-        acc[r][1] += __shfl_xor(acc[r][1], o, kWave);
-      }
-    if (lane < RPW) {
-      float a0 = 0.0f, a1 = 0.0f;
-#pragma unroll
-      for (int r = 0; r < RPW; ++r)
-        if (r == lane) { a0 = acc[r][0]; a1 = acc[r][1]; }
-      const int n = n0 + lane;
-      if (n < n_rows) {
-        mod[n] = a0 + bias[n];
-        if (B > 1) mod[(size_t)n_rows + n] = a1 + bias[n];
-      }
-    }
+  }
+  if (n < n_rows) {
+    mod[n] = a0 + bias[n];
+    if (B > 1) mod[(size_t)n_rows + n] = a1 + bias[n];
   }
 }
 
@@ -283,12 +273,17 @@ static hipError_t launch_cond_t(const CondParams& p, hipStream_t s) {
                      reinterpret_cast<const T*>(p.w_t2), p.b_t2, p.t1,
                      reinterpret_cast<const T*>(p.table), p.hidden, p.B, p.labels[0],
                      p.labels[1], p.sc);
-  constexpr int RPW = 4;
-  const int blocks = min(2048, ceil_div(p.n_mod, 4 * RPW));
-  hipLaunchKernelGGL((adaln_gemv_kernel<T, RPW>), dim3(blocks), dim3(256), 0, s,
+  const int blocks = ceil_div(ceil_div(p.n_mod, kAdaGroup), 4);
+  hipLaunchKernelGGL(adaln_gemv_kernel<T>, dim3(blocks), dim3(256), 0, s,
                      reinterpret_cast<const T*>(p.w_ada), p.b_ada, p.sc, p.hidden, p.n_mod, p.B,
                      p.mod);
   return hipGetLastError();
+}
+
+size_t adaln_group_index(size_t row, size_t col, int H, int esize) {
+  const size_t ch = 16 / esize, nck = H / ch;
+  const size_t g = row / kAdaGroup, l = row % kAdaGroup, k = col / ch;
+  return ((g * nck + k) * kAdaGroup + l) * ch + col % ch;
 }
 
 hipError_t launch_conditioning(const CondParams& p, int dtype, hipStream_t s) {

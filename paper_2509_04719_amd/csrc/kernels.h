@@ -91,7 +91,9 @@ struct CondParams {
   const void* w_t1; const float* b_t1;     // [H][freq], [H]
   const void* w_t2; const float* b_t2;     // [H][H], [H]
   const void* table;                        // [(classes+1)][H]
-  const void* w_ada; const float* b_ada;   // [n_mod][H], [n_mod]
+  // w_ada: [n_mod][H] held in 64-row groups, element (n, c) at
+  // adaln_group_index(n, c, H, element size) (rows past n_mod zero)
+  const void* w_ada; const float* b_ada;   // [n_mod], biases
   int hidden, freq_dim, n_mod, B;
   int labels[2];
   float t;
@@ -100,6 +102,7 @@ struct CondParams {
   float* mod;                               // fp32 [B][n_mod]
 };
 hipError_t launch_conditioning(const CondParams& p, int dtype, hipStream_t stream);
+size_t adaln_group_index(size_t row, size_t col, int H, int esize);
 
 struct PatchEmbedParams {
   const float* x;        // fp32 [C][latent][latent]

@@ -344,15 +344,11 @@ int orch_load_dit_weights(orch_ctx* x, const void* host_blob, size_t nbytes) {
   const size_t o_t1 = wadd(tab[3]);
   const size_t o_t2 = wadd(tab[5]);
   const size_t o_tab = wadd(tab[7]);
-  // adaLN block matrices contiguous: place without padding between them
+  // adaLN: the block matrices and the final one as one [n_mod][H] matrix,
+  // held in the 64-row groups of the conditioning GEMV (copied below)
   const size_t o_ada = woff;
-  for (int l = 0; l < x->L; ++l) {
-    wlist.push_back({&tab[first_block + per_block * l + 0], woff});
-    woff += 6 * H * H;
-  }
   const size_t nb_final = first_block + per_block * x->L;
-  wlist.push_back({&tab[nb_final + 0], woff});
-  woff += 2 * H * H;
+  woff += (size_t)(x->n_mod + 63) / 64 * 64 * H;
   woff = (woff + 127) / 128 * 128;
   std::vector<size_t> o_qkv(x->L), o_proj(x->L), o_fc1(x->L), o_fc2(x->L);
   for (int l = 0; l < x->L; ++l) {
@@ -365,6 +361,20 @@ int orch_load_dit_weights(orch_ctx* x, const void* host_blob, size_t nbytes) {
   const size_t o_final = wadd(tab[nb_final + 2]);
   std::vector<unsigned char> hw(woff * es);
   for (auto& pr : wlist) memcpy(hw.data() + pr.second * es, blob + pr.first->offset, pr.first->count * es);
+  {
+    // adaLN rows: block l's 6H rows, then the final 2H, each row H elements
+    size_t row = 0;
+    auto put = [&](const Tensor& t, size_t rows) {
+      const unsigned char* src = blob + t.offset;
+      const size_t ch = 16 / es;   // elements per 16-byte chunk, kept together
+      for (size_t r = 0; r < rows; ++r, ++row)
+        for (size_t c = 0; c < H; c += ch)
+          memcpy(hw.data() + (o_ada + adaln_group_index(row, c, (int)H, (int)es)) * es,
+                 src + (r * H + c) * es, 16);
+    };
+    for (int l = 0; l < x->L; ++l) put(tab[first_block + per_block * l + 0], 6 * H);
+    put(tab[nb_final + 0], 2 * H);
+  }
 
   // fp32 vectors: biases (adaLN concatenated), patch-embedding weight, position table.
   std::vector<float> hf;
