@@ -235,6 +235,31 @@ def kernel_split(torch, L, cfg, n_q: int, iters: int):
     return out
 
 
+def hbm_kernels(torch, L):
+    """The HBM-bound elementwise kernels at large synthetic shapes, where
+    launch overhead no longer hides the streaming rate: the guided scheduler
+    update over 256 Mi elements (x, both branches' eps in, out: 16 B per
+    element) and the adaLN LayerNorm over 65536 rows of 1152 (fp32 in, bf16
+    out: 6 B per element).  GB/s = algorithmic bytes / average launch time."""
+    dev = "cuda:0"
+    res = {}
+    n = 256 << 20
+    x = torch.randn(n, device=dev)
+    ec, eu = torch.randn(n, device=dev), torch.randn(n, device=dev)
+    out = torch.empty(n, device=dev)
+    ms = _time_loop(torch, lambda: L.scheduler_update(x, ec, eu, 1.5, None, 1.2, 0.2, 0.0, out), 10)
+    res["scheduler_update_256Mi"] = {"us": round(ms * 1e3, 1), "gbs": round(16 * n / ms / 1e6, 1)}
+    del x, ec, eu, out
+    rows, H = 65536, 1152
+    h = torch.randn(rows, H, device=dev)
+    mod = torch.randn(2, 2 * H, device=dev) * 0.1
+    u = torch.empty(rows, H, dtype=torch.bfloat16, device=dev)
+    ms = _time_loop(torch, lambda: L.layernorm_modulate(h, rows, H, rows // 2, mod[:, :H], mod[:, H:],
+                                                       2 * H, u, 1), 10)
+    res["layernorm_65536x1152"] = {"us": round(ms * 1e3, 1), "gbs": round(6 * rows * H / ms / 1e6, 1)}
+    return res
+
+
 def step_kernel_split(ctx, cfg, n_q: int, run_step, steps: int):
     """Per-kernel-class average launch time inside the step itself: every
     launch of `steps` steps bracketed by HIP events on the step's stream
@@ -508,6 +533,9 @@ def main(argv=None) -> int:
         print(f"# kernel-level entry points: {json.dumps(kernel_split(torch, L, cfg, n_q, a.kernel_iters))}",
               flush=True)
 
+    hbm = hbm_kernels(torch, L)
+    print(f"# HBM-bound kernels at large shapes: {json.dumps(hbm)}", flush=True)
+
     sweep = {}
     if a.sweep:
         for share in (0.10, 0.25, 0.40, 0.65, 1.00):
@@ -541,6 +569,7 @@ def main(argv=None) -> int:
         "attn_gemm_frac": round(mfma_flops / mfma_ms / 1e9 / PEAK_BF16_TFLOPS, 4),
         "roofline": roofline,
         "kernels": split,
+        "hbm_kernels": hbm,
         "share_sweep": sweep,
         "cpu_baseline": cpu,
     }
