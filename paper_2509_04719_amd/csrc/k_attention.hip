@@ -2,17 +2,19 @@
 // fresh for the band's tokens and stale (from the buffer) for all others
 // (patch parallelism with stale activations, §II-B; Algorithm 1).
 //
-// bf16 path: a flash-style kernel on v_mfma_f32_32x32x16_bf16.  Each
-// workgroup owns 128 queries of one (branch, head); each wave 32 of them.
-// Scores are formed transposed, S^T = K Q^T, so that a lane owns one query
-// column: the running max of the online softmax stays in-lane, and the
-// probabilities it holds are directly the B operand of O^T = V^T P^T.
+// bf16 path: a flash-style kernel on the matrix cores.  Each workgroup owns
+// 128 queries of one (branch, head); each wave 32 of them.  Scores are formed
+// transposed on v_mfma_f32_32x32x16_bf16, S^T = K Q^T, so that a lane owns one
+// query column and the running max of the online softmax stays in-lane.
+// O^T = V^T P^T runs on v_mfma_f32_16x16x32_bf16 (16-row tiles of O^T: d = 72
+// pads to 80 rows, not 96); two lane swaps move the probabilities from the
+// score layout into its B operand.
 // K tiles ([64 keys][d], rows unpadded) and V^T tiles ([d][64 keys], 16-byte
 // chunks XOR-swizzled by row) go global -> LDS with the direct-to-LDS load
-// into a ring of three stages, one barrier per tile.  K rows are permuted in
+// into a ring of four stages, one barrier per tile.  K rows are permuted in
 // LDS (bits 2 and 3 of the row swapped) so that the 8 keys of each lane's P
 // fragment are contiguous in natural key order.  When the head dimension is
-// padded (d = 72 -> 96 rows of O^T), one padding row of V^T holds ones, so
+// padded (d = 72 -> 80 rows of O^T), one padding row of V^T holds ones, so
 // the PV product also accumulates the softmax denominator.  exp2 runs on
 // v_exp_f32 with log2(e)/sqrt(d) folded into the exponent; the running max is
 // raised lazily (only past a 2^8 margin), so O is rarely rescaled.  The loop
@@ -37,8 +39,8 @@ template <int D>
 struct Geo {
   static constexpr int NC = (D + 15) / 16;          // 16-dim chunks of S^T = K Q^T
   static constexpr int NS = 2 * NC;                 // MFMAs of one S^T tile
-  static constexpr int DV = (D + 31) / 32 * 32;     // rows of O^T, padded to 32
-  static constexpr int NT = DV / 32;
+  static constexpr int DV = (D + 15) / 16 * 16;     // rows of O^T, padded to 16
+  static constexpr int NT = DV / 16;                // 16-row tiles of O^T
   static constexpr bool ONES = DV > D;              // padding row D of V^T holds 1.0
   // d = 8 (mod 16): the upper half of the last 16-dim chunk is padding, where
   // K reads the constant (1, 1, 1, 0, ...) and Q carries -m_run split in three
@@ -217,18 +219,21 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
     else wait_vmcnt<2 * LPW>();
   };
 
-  // fragment read offsets: K row sub*32 + lc, logical chunk 2c + h; V^T row
-  // t*32 + lc, logical chunk 2c + h (the swizzle depends on lc only).  V^T
-  // rows >= D are the shared constant rows.
+  // fragment read offsets: K row sub*32 + lc, logical chunk 2c + h (A of the
+  // 32x32x16 MFMA: row lane & 31, k 8 (lane >> 5) .. +8); V^T row 16 t + r16,
+  // logical chunk 4 psub + (lane >> 4) (A of the 16x16x32 MFMA: row lane & 15,
+  // k 8 (lane >> 4) .. +8; the swizzle depends on r16 only).  V^T rows >= D
+  // are the shared constant rows.
   // (unswizzled rows: one base, the chunks at immediate offsets 32 c)
   int k_rd[G::KSWZ ? NC : 1];
 #pragma unroll
   for (int c = 0; c < (G::KSWZ ? NC : 1); ++c)
     k_rd[c] = lc * G::KROW + (G::KSWZ ? ((2 * c + h) ^ ((lc >> 1) & 7)) : (2 * c + h)) * 16;
-  int v_rd[4];
+  const int r16 = lane & 15, g16 = lane >> 4;
+  int v_rd[2];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) v_rd[c] = lc * G::VROW + ((2 * c + h) ^ ((lc >> 1) & 7)) * 16;
-  const bool last_in_pad = (NT - 1) * 32 + lc >= D;   // row of the last O^T tile is padding
+  for (int ps = 0; ps < 2; ++ps) v_rd[ps] = r16 * G::VROW + ((4 * ps + g16) ^ ((r16 >> 1) & 7)) * 16;
+  const bool last_in_pad = (NT - 1) * 16 + r16 >= D;   // row of the last O^T tile is padding
   // the last K chunk of half sub: the max column's constant on the h = 1 lanes
   int k_last[2];
 #pragma unroll
@@ -238,7 +243,24 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
 
   const float scale = 1.4426950408889634f / sqrtf((float)D);  // log2(e) / sqrt(d)
   float m_run, l_run;
-  f32x16 o[NT];
+  // O^T tile t (rows 16 t .. +16) of the queries 16 j + (lane & 15) is the
+  // 4-float accumulator f = 2 t + j, elements 4 (f % 4) .. +4 of oo[f / 4].
+  // (As separate 4-float values the register allocator moved every one of
+  // them between two register sets each half-step: 65 copies per tile and
+  // 54 more registers; held in 16-float tuples they stay in place.)
+  f32x16 oo[(2 * NT + 3) / 4];
+  auto oget = [&](int t, int j) __attribute__((always_inline)) {
+    const int f = 2 * t + j;
+    f32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = oo[f / 4][4 * (f % 4) + i];
+    return r;
+  };
+  auto oset = [&](int t, int j, const f32x4& r) __attribute__((always_inline)) {
+    const int f = 2 * t + j;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) oo[f / 4][4 * (f % 4) + i] = r[i];
+  };
   f32x16 negm;   // without the max column: -m_run in every element, the input of each score chain
   const f32x16 zero16 = {};
   // -m_run into the max column of Q (h = 1 lanes, last chunk): three bf16
@@ -270,20 +292,40 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
       kf_[c] = *reinterpret_cast<const bf16x8*>(sk + (G::KSWZ ? k_rd[c] : k_rd[0] + 32 * c));
     kf_[NC - 1] = *reinterpret_cast<const bf16x8*>(smem + st * G::STAGE + (sub ? k_last[1] : k_last[0]));
   };
-  // V^T fragment of O^T tile tt and 16-key chunk c of the tile in stage st
-  auto v_frag = [&](int st, int tt, int c) {
+  // V^T fragment of O^T tile tt, keys of half ps, of the tile in stage st
+  auto v_frag = [&](int st, int tt, int ps) {
     const char* src = (tt == NT - 1 && last_in_pad)
-                          ? smem + G::CONST_OFF + (tt * 32 + lc - D) * G::VROW + (v_rd[c] - lc * G::VROW)
-                          : smem + st * G::STAGE + G::K_SPAN + tt * 32 * G::VROW + v_rd[c];
+                          ? smem + G::CONST_OFF + (tt * 16 + r16 - D) * G::VROW + (v_rd[ps] - r16 * G::VROW)
+                          : smem + st * G::STAGE + G::K_SPAN + tt * 16 * G::VROW + v_rd[ps];
     return *reinterpret_cast<const bf16x8*>(src);
+  };
+  // P^T of a 32-key half from the score layout (16-key chunk ci, lane half h:
+  // keys 16 ci + 8 h .. +8 of query lane & 31) into the B layout of the
+  // 16x16x32 MFMA (pq[j], lane l: keys 8 (l >> 4) .. +8 of query 16 j +
+  // (l & 15)).  In 16-lane rows, chunk 0 = (a0 a1 a2 a3) and chunk 1 =
+  // (b0 b1 b2 b3): the 32-lane swap gives (a0 a1 b0 b1) and (a2 a3 b2 b3), the
+  // 16-lane swap then (a0 a2 b0 b2) = queries 0-15 and (a1 a3 b1 b3) = 16-31.
+  auto p_swap = [&](bf16x8(&pp)[2]) __attribute__((always_inline)) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 x = __builtin_bit_cast(u32x4, pp[0]), y = __builtin_bit_cast(u32x4, pp[1]);
+    u32x4 q0, q1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const auto r = __builtin_amdgcn_permlane32_swap(x[i], y[i], false, false);
+      const auto t = __builtin_amdgcn_permlane16_swap(r[0], r[1], false, false);
+      q0[i] = t[0];
+      q1[i] = t[1];
+    }
+    pp[0] = __builtin_bit_cast(bf16x8, q0);
+    pp[1] = __builtin_bit_cast(bf16x8, q1);
   };
 
   // One 32-key half of the stream of key tiles.  sc: S^T of keys [32 sub,
   // +32) of the tile in stage st.  Its exponentials are interleaved with the
   // MFMAs of the next half's scores (NEXT: K fragments of stage nst, half
   // nsub, into sn) and of the previous half's O^T += V^T P^T (probabilities
-  // pp, V^T of stage pst, half psub), so a wave keeps its matrix core busy
-  // through the softmax.  This half's probabilities go to pc.
+  // pp in the score layout, V^T of stage pst, half psub), so a wave keeps its
+  // matrix core busy through the softmax.  This half's probabilities go to pc.
   auto step = [&](auto next_c, bool start, int st, int sub, f32x16& sc, int nst, int nsub,
                   f32x16& sn, int pst, int psub, bf16x8(&pp)[2], bf16x8(&pc)[2]) {
     constexpr bool NEXT = decltype(next_c)::value;
@@ -296,14 +338,14 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
     // then exp2(sc) <= 2^8, exact in fp32 and in range for bf16, so O is
     // rarely rescaled; when it is, by a power of two, which scales the
     // previous half's pending probabilities exactly too.  The fragment reads
-    // go first, in order of use; the max below covers their latency.
-    bf16x8 vp[2][NT];
+    // go first, in order of use; the lane swaps and the max below cover their
+    // latency.
+    bf16x8 vp[NT];
 #pragma unroll
-    for (int ci = 0; ci < 2; ++ci)
-#pragma unroll
-      for (int tt = 0; tt < NT; ++tt) vp[ci][tt] = v_frag(pst, tt, 2 * psub + ci);
+    for (int tt = 0; tt < NT; ++tt) vp[tt] = v_frag(pst, tt, psub);
     bf16x8 kn[NC];
     if constexpr (NEXT) k_frags(nst, nsub, kn);
+    p_swap(pp);   // pp[j]: queries 16 j .. +16
     // a chain of three-way maxima (v_max3_f32: two new values each)
     float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
 #pragma unroll
@@ -324,14 +366,19 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
 #pragma unroll
         for (int r = 0; r < 16; ++r) negm[r] = -m_run;
       }
+      // O^T and the swapped probabilities hold queries 16 j + (lane & 15)
+      float aj[2];
 #pragma unroll
-      for (int tt = 0; tt < NT; ++tt)
+      for (int j = 0; j < 2; ++j) aj[j] = __shfl(alpha, 16 * j + r16, kWave);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[tt][r] *= alpha;
+      for (int j = 0; j < 2; ++j) {
 #pragma unroll
-      for (int ci = 0; ci < 2; ++ci)
+        for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pp[ci][e] = (bf16)((float)pp[ci][e] * alpha);
+          for (int r = 0; r < 4; ++r) oo[(2 * tt + j) / 4][4 * ((2 * tt + j) % 4) + r] *= aj[j];   // oget(tt, j) *= aj[j]
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pp[j][e] = (bf16)((float)pp[j][e] * aj[j]);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     // the MFMA-dense part runs at raised wave priority: the two waves sharing a
@@ -339,9 +386,9 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
     // MFMAs (measured 3-4% faster than equal priorities)
     __builtin_amdgcn_s_setprio(1);
     float psum = 0.0f;
-    // per 16-key chunk ci: NM MFMAs (PV and S alternating, PV first) in
-    // groups, each followed by its share of the chunk's 4 pairs of
-    // exponentials; a scheduling fence after each group keeps the order
+    // per 16-key chunk ci: NM MFMAs (PV of query block ci and S alternating,
+    // PV first) in groups, each followed by its share of the chunk's 4 pairs
+    // of exponentials; a scheduling fence after each group keeps the order
     static_for<0, 2>([&](auto cc) {
       constexpr int ci = decltype(cc)::value;
       constexpr int c0 = ci * NC / 2, c1 = (ci + 1) * NC / 2;
@@ -351,7 +398,7 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
         constexpr bool pv = g < 2 * NB ? g % 2 == 0 : NT > NSM;
         constexpr int idx = g < 2 * NB ? g / 2 : g - NB;
         if constexpr (pv)
-          o[idx] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[ci][idx], pp[ci], o[idx], 0, 0, 0);
+          oset(idx, ci, __builtin_amdgcn_mfma_f32_16x16x32_bf16(vp[idx], pp[ci], oget(idx, ci), 0, 0, 0));
         else
           sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kn[c0 + idx], qf[c0 + idx],
                                                       c0 + idx == 0 ? chain_in() : sn, 0, 0, 0);
@@ -437,9 +484,9 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
     }
     l_run = 0.0f;
 #pragma unroll
-    for (int tt = 0; tt < NT; ++tt)
+    for (int k = 0; k < (2 * NT + 3) / 4; ++k)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[tt][r] = 0.0f;
+      for (int r = 0; r < 16; ++r) oo[k][r] = 0.0f;
 
 #pragma unroll
     for (int s = 0; s < NSTAGE - 1; ++s)
@@ -479,52 +526,60 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
       step(std::true_type{}, t == 0, st, 0, s0, st, 1, s1, pst, t == 0 ? 0 : 1, pa, pb);
       step(std::false_type{}, false, st, 1, s1, 0, 0, s0, st, 0, pb, pa);
       // the last half's PV
-      bf16x8 vp[2][NT];
+      bf16x8 vp[NT];
 #pragma unroll
-      for (int ci = 0; ci < 2; ++ci)
+      for (int tt = 0; tt < NT; ++tt) vp[tt] = v_frag(st, tt, 1);
+      p_swap(pa);
 #pragma unroll
-        for (int tt = 0; tt < NT; ++tt) vp[ci][tt] = v_frag(st, tt, 2 + ci);
-#pragma unroll
-      for (int ci = 0; ci < 2; ++ci)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt)
-          o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp[ci][tt], pa[ci], o[tt], 0, 0, 0);
+          oset(tt, j, __builtin_amdgcn_mfma_f32_16x16x32_bf16(vp[tt], pa[j], oget(tt, j), 0, 0, 0));
     }
 
-    // softmax denominator: the ones row D of O^T (register 4*((D%32)/8) + D%4
-    // of tile D/32 on the h == 0 lanes), or the running sum
-    float l;
+    // softmax denominator of query 16 j + (lane & 15): the ones row D of O^T
+    // (tile D / 16, register (D % 16) % 4 of the lanes 16 ((D % 16) / 4) ..
+    // +16), or the running sums of the query's two lane halves
+    float lj[2];
     if constexpr (G::ONES) {
-      constexpr int TR = D / 32, RR = 4 * ((D % 32) / 8) + (D % 4);
-      static_assert(((D % 32) / 4) % 2 == 0, "ones row on the h == 0 half");
-      l = __shfl(o[TR][RR], lc, kWave);
+      constexpr int TR = D / 16, RG = (D % 16) / 4, RR = (D % 16) % 4;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) lj[j] = __shfl(oget(TR, j)[RR], 16 * RG + r16, kWave);
     } else {
-      l = l_run + __shfl_xor(l_run, 32, kWave);
+      const float lq = l_run + __shfl_xor(l_run, 32, kWave);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) lj[j] = __shfl(lq, 16 * j + r16, kWave);
     }
     // a whole query tile goes to the output; the part of a cut one to this
     // workgroup's slot (2w: the first tile of its range, 2w + 1: the last) as
-    // O_s / l_s in bf16 with (max, sum), for the merge
-    const int ql = wave * 32 + lc, q = q0 + ql;
+    // O_s / l_s in bf16 with (max, sum), for the merge.  A lane holds dims
+    // 16 t + 4 (lane >> 4) .. +4 of queries 16 j + (lane & 15).
     const bool whole = a == 0 && bnd == nkt;
     const int slot = 2 * w + (tile == tile_first ? 0 : 1);
-    const float inv = 1.0f / l;
-    if (q < p.n_q) {
-      bf16* orow = whole ? reinterpret_cast<bf16*>(p.out) + ((size_t)b * p.n_q + q) * H + head * D
-                         : reinterpret_cast<bf16*>(p.part_o) + ((size_t)slot * BQ + ql) * D;
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+    for (int j = 0; j < 2; ++j) {
+      const int ql = wave * 32 + 16 * j + r16, q = q0 + ql;
+      const float inv = 1.0f / lj[j];
+      if (q < p.n_q) {
+        bf16* orow = whole ? reinterpret_cast<bf16*>(p.out) + ((size_t)b * p.n_q + q) * H + head * D
+                           : reinterpret_cast<bf16*>(p.part_o) + ((size_t)slot * BQ + ql) * D;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int d = t * 32 + 8 * g + 4 * h;
+        for (int t = 0; t < NT; ++t) {
+          const int d = 16 * t + 4 * g16;
           if (d < D) {
             bf16x4 v;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[t][4 * g + j] * inv);
+            for (int i = 0; i < 4; ++i) v[i] = (bf16)(oget(t, j)[i] * inv);
             *reinterpret_cast<bf16x4*>(orow + d) = v;
           }
         }
-      if (!whole && h == 0) p.part_ml[(size_t)slot * BQ + ql] = make_float2(m_run, l);
+      }
     }
+    // (max, sum) of the query lane & 31 of the score layout, whose sum is
+    // lj[(lane & 31) >> 4] here
+    const int ql = wave * 32 + lc;
+    if (!whole && h == 0 && q0 + ql < p.n_q)
+      p.part_ml[(size_t)slot * BQ + ql] = make_float2(m_run, lc >> 4 ? lj[1] : lj[0]);
   }
 #endif
 }
