@@ -590,16 +590,24 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
 // with m = max_s m_s.  One thread per 8 channels of a query; grid (chunk
 // groups, query tiles).  The parts are taken four at a time with their loads
 // issued together (a tile is cut into two or three parts in the common
-// case), merged online.  Tiles computed whole return at once.
+// case), merged online.  Tiles computed whole return at once.  A tile's
+// 128 x D / 8 threads fill whole workgroups (three of 384 for d = 72).
 template <int D>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+struct MergeGeo {
+  static constexpr int CPQ = D / 8;                // 16-byte chunks per query
+  static constexpr int THREADS = mfma_attn::BQ * CPQ % 384 == 0 ? 384 : 256;
+  static constexpr int BLOCKS = (mfma_attn::BQ * CPQ + THREADS - 1) / THREADS;
+};
+
+template <int D>
+__global__ __launch_bounds__(MergeGeo<D>::THREADS) void attn_merge_kernel(AttnParams p) {
   using namespace mfma_attn;
-  constexpr int CPQ = D / 8;                       // 16-byte chunks per query
+  constexpr int CPQ = MergeGeo<D>::CPQ;
   const int nkt = p.n_kv / BKV, n_qt = (p.n_q + BQ - 1) / BQ;
   const int tile = blockIdx.y;
   const int w0 = tile * nkt / p.per, w1 = (tile * nkt + nkt - 1) / p.per;
   if (w0 == w1) return;
-  const int i = blockIdx.x * 256 + threadIdx.x;
+  const int i = blockIdx.x * MergeGeo<D>::THREADS + threadIdx.x;
   const int ql = i / CPQ, c = i - ql * CPQ;
   const int qt = tile % n_qt, pair = tile / n_qt;
   const int q = qt * BQ + ql;
@@ -794,11 +802,12 @@ hipError_t launch_attention(const AttnParams& p0, int dtype, hipStream_t s) {
     else
       launch_mfma<72>(dim3(p.workers), p, s);
     if (cut) {
-      const dim3 g2(ceil_div(mfma_attn::BQ * p.d / 8, 256), tiles);
       if (p.d == 64)
-        hipLaunchKernelGGL(attn_merge_kernel<64>, g2, dim3(256), 0, s, p);
+        hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(MergeGeo<64>::BLOCKS, tiles),
+                           dim3(MergeGeo<64>::THREADS), 0, s, p);
       else
-        hipLaunchKernelGGL(attn_merge_kernel<72>, g2, dim3(256), 0, s, p);
+        hipLaunchKernelGGL(attn_merge_kernel<72>, dim3(MergeGeo<72>::BLOCKS, tiles),
+                           dim3(MergeGeo<72>::THREADS), 0, s, p);
     }
     return hipGetLastError();
   }
