@@ -302,7 +302,11 @@ struct StripEpilogue {
       }
     }
     // V^T [head][d][token]: 8 consecutive tokens of one channel per lane;
-    // four lanes cover the strip's 32 tokens (64 contiguous bytes)
+    // four lanes cover the strip's 32 tokens (64 contiguous bytes).  Token
+    // groups 2 and 3 read their tokens rotated by four (8 LS = 32 mod 64 banks
+    // would put them on the banks of groups 0 and 1; 4 LS = 16 mod 64 moves
+    // them to the free ones), then swap the halves back.
+    static_assert((4 * LS) % 64 == 16, "conflict-free V^T reads");
     if (n0 + TN > 2 * hidden) {
       constexpr int IT = TN * 4 / 64;
 #pragma unroll
@@ -310,9 +314,19 @@ struct StripEpilogue {
         const int col = q * 16 + (lane >> 2), grp = lane & 3;
         const int n = n0 + col;
         if (n < 2 * hidden) continue;
+        const int rot = (grp >> 1) * 4;
         float v[8];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) v[t] = strip[(grp * 8 + t) * LS + col];
+        for (int t = 0; t < 8; ++t) {
+          const float x = strip[(grp * 8 + ((t + rot) & 7)) * LS + col];   // token t ^ rot
+          v[t] = x;
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const float a = v[t], b = v[t + 4];
+          v[t] = rot ? b : a;
+          v[t + 4] = rot ? a : b;
+        }
         const float bias = pre.vb[q];
         const int nn = n - 2 * hidden, head = (int)__umulhi((unsigned)nn, ep.hd_magic), dd = nn - head * hd;
         bf16* vt = kvb + ntot * hidden + ((size_t)head * hd + dd) * ntot + ep.tok_offset;
