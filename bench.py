@@ -448,7 +448,7 @@ def main(argv=None) -> int:
     ap.add_argument("--m-base", type=int, default=50)
     ap.add_argument("--m-warmup", type=int, default=10)
     ap.add_argument("--thr-a", type=float, default=0.75)
-    ap.add_argument("--thr-b", type=float, default=0.3)
+    ap.add_argument("--thr-b", type=float, default=0.25)
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run the workload of the HBM counter runs and exit")
     ap.add_argument("--pmc-report", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),

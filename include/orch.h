@@ -157,13 +157,15 @@ int orch_schedule_coefficients(const orch_dit_config* cfg, int t, int t_prev, do
 /* Host only: the device plan of the method for n devices of effective speed
  * speed[i] > 0 (for example c_i (1 - rho_i): capability times idle share).
  * Temporal adaptation (Eq. (2)): with v_max = max speed, device i keeps
- * m_base steps when a*v_max < speed[i], the reduced tier m_base/2 +
- * m_warmup/2 (integer halves) when b*v_max < speed[i] <= a*v_max, and is
- * excluded (0 steps, 0 rows) otherwise; 0 < b < a < 1.  Spatial adaptation
- * (Eq. (3)): device i gets the share (v_i/M_i) / sum_j (v_j/M_j) of
- * total_rows token rows, rounded to whole rows by largest remainders (ties
- * to the lower index), so the rows sum to total_rows.  steps_out and
- * rows_out are host arrays of n ints.  Errors: ORCH_EINVAL. */
+ * m_base steps when a*v_max < speed[i], the reduced tier
+ * ceil((m_base + m_warmup) / 2) when b*v_max < speed[i] <= a*v_max (m_warmup
+ * single steps, then the rest of the grid in steps of two intervals), and is
+ * excluded (0 steps, 0 rows) otherwise; 0 < b < a < 1 (the evaluation of
+ * §V-A uses a = 0.75, b = 0.25).  Spatial adaptation (Eq. (3)): device i gets
+ * the share (v_i/M_i) / sum_j (v_j/M_j) of total_rows token rows, rounded to
+ * whole rows by largest remainders (ties to the lower index), so the rows sum
+ * to total_rows; a device whose share rounds to no rows gets 0 steps.
+ * steps_out and rows_out are host arrays of n ints.  Errors: ORCH_EINVAL. */
 int orch_plan_devices(const double* speed, int n, int m_base, int m_warmup, double a, double b,
                       int total_rows, int* steps_out, int* rows_out);
 

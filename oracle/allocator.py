@@ -5,7 +5,8 @@ TEST INFRASTRUCTURE ONLY -- see the package docstring.
 Temporal adaptation (Eq. (2), §III-C): with v_max the largest effective
 speed, a device keeps M_base steps when a*v_max < v_i, takes the reduced tier
 M_base/2 + M_warmup/2 when b*v_max < v_i <= a*v_max, and is excluded when
-v_i <= b*v_max (0 < b < a < 1).
+v_i <= b*v_max (0 < b < a < 1).  The evaluation (§V-A) uses a = 0.75,
+b = 0.25.
 
 Spatial adaptation, patch mending (Eq. (3), §III-D): device i gets the share
 (v_i/M_i) / sum_j (v_j/M_j) of the image, over the devices not excluded.
@@ -13,8 +14,12 @@ Spatial adaptation, patch mending (Eq. (3), §III-D): device i gets the share
 Readings (the paper leaves these open):
   * The effective speed is v_i = c_i * (1 - rho_i) (capability times idle
     fraction); the planner also takes v directly.
-  * The reduced tier has M_base // 2 + M_warmup // 2 steps (integer halves;
-    Table II's 100:52 and 50:27 at M_warmup = 4).
+  * The reduced tier has ceil((M_base + M_warmup) / 2) steps: M_warmup single
+    steps, then the rest of the grid in steps of two intervals, the last one
+    single when M_base - M_warmup is odd -- the count the reduced-tier
+    schedule executes (Table II's 100:52 and 50:27 at M_warmup = 4; 63 for
+    M_base = 100, M_warmup = 25).
+  * A device whose share rounds to no rows has no work: it runs 0 steps.
   * Shares are turned into whole token rows by largest remainders: each device
     gets floor(P_i), the rows left over go to the largest fractional parts,
     ties to the lower index; the rows always sum to P_total.
@@ -29,6 +34,11 @@ def effective_speed(c: float, rho: float) -> float:
     return c * (1.0 - rho)
 
 
+def reduced_steps(M_base: int, M_warmup: int) -> int:
+    """Eq. (2), middle case: M_warmup single steps, then ceil of half the rest."""
+    return M_warmup + (M_base - M_warmup + 1) // 2
+
+
 def step_counts(v: Sequence[float], M_base: int, M_warmup: int, a: float, b: float) -> List[int]:
     """Eq. (2): steps per device, 0 for an excluded device."""
     vmax = max(v)
@@ -37,7 +47,7 @@ def step_counts(v: Sequence[float], M_base: int, M_warmup: int, a: float, b: flo
         if vi > a * vmax:
             out.append(M_base)
         elif vi > b * vmax:
-            out.append(M_base // 2 + M_warmup // 2)
+            out.append(reduced_steps(M_base, M_warmup))
         else:
             out.append(0)
     return out
@@ -66,4 +76,5 @@ def plan(v: Sequence[float], M_base: int, M_warmup: int, a: float, b: float, tot
     """(steps, rows) per device: Eq. (2) then Eq. (3) in whole rows."""
     steps = step_counts(v, M_base, M_warmup, a, b)
     rows = whole_rows(patch_shares(v, steps), total_rows)
+    steps = [m if r > 0 else 0 for m, r in zip(steps, rows)]
     return steps, rows

@@ -100,8 +100,11 @@ def step_pairs(T: int, M: int) -> List[Tuple[int, int]]:
 
 
 def tiered_step_count(M_base: int, M_warmup: int) -> int:
-    """Eq. (2), middle case: steps of a device in the reduced tier."""
-    return M_base // 2 + M_warmup // 2
+    """Eq. (2), middle case: steps of a device in the reduced tier,
+    M_base/2 + M_warmup/2 rounded up -- M_warmup single steps, then the rest
+    of the grid in steps of two intervals (the last one single when
+    M_base - M_warmup is odd)."""
+    return -(-(M_base + M_warmup) // 2)
 
 
 def tiered_schedule(T: int, M_base: int, M_warmup: int

@@ -26,11 +26,13 @@ int orch_plan_devices(const double* speed, int n, int m_base, int m_warmup, doub
       return set_error(ORCH_EINVAL, "speeds must be finite and > 0");
     vmax = std::max(vmax, speed[i]);
   }
-  // Eq. (2): full, reduced (M_base/2 + M_warmup/2) or excluded
+  // Eq. (2): full, reduced or excluded.  The reduced tier runs m_warmup
+  // single steps, then the rest of the grid in steps of two intervals (the
+  // last one single when m_base - m_warmup is odd): ceil((m_base + m_warmup)/2).
   std::vector<int> steps(n);
   for (int i = 0; i < n; ++i) {
     if (speed[i] > a * vmax) steps[i] = m_base;
-    else if (speed[i] > b * vmax) steps[i] = m_base / 2 + m_warmup / 2;
+    else if (speed[i] > b * vmax) steps[i] = m_warmup + (m_base - m_warmup + 1) / 2;
     else steps[i] = 0;
   }
   // Eq. (3): share of device i = (v_i/M_i) / sum_j (v_j/M_j)
@@ -55,8 +57,9 @@ int orch_plan_devices(const double* speed, int n, int m_base, int m_warmup, doub
     ++rows[best];
     frac[best] = -1.0;
   }
+  // a device left with no rows has no work
   for (int i = 0; i < n; ++i) {
-    steps_out[i] = steps[i];
+    steps_out[i] = rows[i] > 0 ? steps[i] : 0;
     rows_out[i] = rows[i];
   }
   return ORCH_OK;

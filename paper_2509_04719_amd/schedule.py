@@ -5,7 +5,8 @@
 * Reduced tier of the tiered step reduction (Algorithm 1, slow branch; Eq. (2)
   middle case): the first M_warmup grid steps run one by one, then steps of
   two grid intervals (Theorem 2 with n = 2) until the end; the buffer is
-  refreshed on every executed step.  That gives M_base/2 + M_warmup/2 steps.
+  refreshed on every executed step.  That gives ceil((M_base + M_warmup)/2)
+  steps (Eq. (2)'s M_base/2 + M_warmup/2, rounded up).
 """
 from __future__ import annotations
 

@@ -101,18 +101,22 @@ def test_library_plan_matches_oracle_exactly(orch_lib):
 
 def test_library_plan_reproduces_quality_tables(orch_lib):
     # two GPUs, 32 units, M_base 100, M_warmup 4, v = 1 - occupancy
-    assert orch_lib.plan_devices([1.0, 0.8], 100, 4, 0.75, 0.3, 32) == ([100, 100], [18, 14])
-    assert orch_lib.plan_devices([1.0, 0.6], 100, 4, 0.75, 0.3, 32) == ([100, 52], [15, 17])
-    assert orch_lib.plan_devices([0.65, 0.55], 100, 4, 0.75, 0.3, 32) == ([100, 100], [17, 15])
-    assert orch_lib.plan_devices([0.7, 0.5], 100, 4, 0.75, 0.3, 32) == ([100, 52], [13, 19])
-    assert orch_lib.plan_devices([1.0, 0.5], 50, 4, 0.75, 0.3, 32)[0] == [50, 27]
+    assert orch_lib.plan_devices([1.0, 0.8], 100, 4, 0.75, 0.25, 32) == ([100, 100], [18, 14])
+    assert orch_lib.plan_devices([1.0, 0.6], 100, 4, 0.75, 0.25, 32) == ([100, 52], [15, 17])
+    assert orch_lib.plan_devices([0.65, 0.55], 100, 4, 0.75, 0.25, 32) == ([100, 100], [17, 15])
+    assert orch_lib.plan_devices([0.7, 0.5], 100, 4, 0.75, 0.25, 32) == ([100, 52], [13, 19])
+    assert orch_lib.plan_devices([1.0, 0.5], 50, 4, 0.75, 0.25, 32)[0] == [50, 27]
+    # Table IV's warm-up of 25 at M_base 100: 25 single steps + 38 double
+    assert orch_lib.plan_devices([1.0, 0.5], 100, 25, 0.75, 0.25, 32)[0] == [100, 63]
+    # a device whose share rounds to no rows runs no steps
+    assert orch_lib.plan_devices([1.0, 1.0, 0.3], 50, 4, 0.75, 0.25, 2) == ([50, 50, 0], [1, 1, 0])
 
 
 @pytest.mark.parametrize("args,word", [
-    (([1.0, -0.5], 50, 4, 0.75, 0.3, 32), "speeds"),
-    (([1.0], 50, 60, 0.75, 0.3, 32), "m_warmup"),
-    (([1.0], 50, 4, 0.3, 0.75, 32), "0 < b < a < 1"),
-    (([1.0], 50, 4, 0.75, 0.3, 0), "total_rows"),
+    (([1.0, -0.5], 50, 4, 0.75, 0.25, 32), "speeds"),
+    (([1.0], 50, 60, 0.75, 0.25, 32), "m_warmup"),
+    (([1.0], 50, 4, 0.25, 0.75, 32), "0 < b < a < 1"),
+    (([1.0], 50, 4, 0.75, 0.25, 0), "total_rows"),
 ])
 def test_library_plan_rejects_bad_arguments(orch_lib, args, word):
     with pytest.raises(orch_lib.OrchError) as e:

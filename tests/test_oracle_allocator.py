@@ -22,7 +22,7 @@ def test_table1_assignments(row):
     """Quality table: patch units and reduced tier from occupancies (v = 1 - rho)."""
     o0, o1, p0, p1, red = row
     v = [al.effective_speed(1.0, o0 / 100), al.effective_speed(1.0, o1 / 100)]
-    steps, rows = al.plan(v, 100, 4, a=0.75, b=0.3, total_rows=32)
+    steps, rows = al.plan(v, 100, 4, a=0.75, b=0.25, total_rows=32)
     assert rows == [p0, p1]
     assert steps == [100, 52 if red else 100]
 
@@ -30,20 +30,40 @@ def test_table1_assignments(row):
 @pytest.mark.parametrize("M_base,expect", [(100, 52), (50, 27)])
 def test_table2_step_counts(M_base, expect):
     """Quality table II: a reduced device runs 100:52 and 50:27 steps (M_warmup = 4)."""
-    assert al.step_counts([1.0, 0.5], M_base, 4, a=0.75, b=0.3) == [M_base, expect]
+    assert al.step_counts([1.0, 0.5], M_base, 4, a=0.75, b=0.25) == [M_base, expect]
 
 
 def test_thresholds_and_exclusion():
-    v = [1.0, 0.9, 0.75, 0.5, 0.3, 0.29]
-    steps = al.step_counts(v, 50, 10, a=0.75, b=0.3)
+    v = [1.0, 0.9, 0.75, 0.5, 0.25, 0.2]
+    steps = al.step_counts(v, 50, 10, a=0.75, b=0.25)
     # a*vmax < v keeps M_base; b*vmax < v <= a*vmax reduced; v <= b*vmax excluded
     assert steps == [50, 50, 30, 30, 0, 0]
-    steps, rows = al.plan(v, 50, 10, 0.75, 0.3, 64)
+    steps, rows = al.plan(v, 50, 10, 0.75, 0.25, 64)
     assert rows[4] == rows[5] == 0 and sum(rows) == 64
 
 
+def test_reduced_count_equals_executed_schedule():
+    """Eq. (2)'s reduced count is the number of steps the reduced tier runs
+    (odd M_base - M_warmup included: Table IV's M_warmup = 25 at M_base = 100)."""
+    from oracle import schedule
+    for mb in range(1, 121):
+        for mw in range(0, mb + 1):
+            n = len(schedule.tiered_schedule(1000, mb, mw)) if mb <= 1000 else None
+            assert al.reduced_steps(mb, mw) == n == schedule.tiered_step_count(mb, mw), (mb, mw)
+    assert al.reduced_steps(100, 25) == 63
+
+
+def test_device_without_rows_has_no_steps():
+    """A device kept by Eq. (2) whose Eq. (3) share rounds to 0 rows has no work."""
+    v = [1.0, 1.0, 0.3]                      # reduced tier, 0.43 of 2 rows
+    assert al.step_counts(v, 50, 4, 0.75, 0.25) == [50, 50, 27]
+    assert al.plan(v, 50, 4, 0.75, 0.25, 2) == ([50, 50, 0], [1, 1, 0])
+    # equal devices, fewer rows than devices: the last ones get none
+    assert al.plan([1.0] * 6, 50, 10, 0.75, 0.25, 4) == ([50] * 4 + [0] * 2, [1] * 4 + [0] * 2)
+
+
 def test_equal_devices_split_evenly():
-    steps, rows = al.plan([0.7] * 4, 50, 10, 0.75, 0.3, 64)
+    steps, rows = al.plan([0.7] * 4, 50, 10, 0.75, 0.25, 64)
     assert steps == [50] * 4 and rows == [16] * 4
 
 
@@ -51,7 +71,7 @@ def test_mending_equalises_rate():
     """Eq. (3): (v_i/M_i)/P_i is the same for every device (before rounding)."""
     rng = np.random.default_rng(0)
     v = list(rng.uniform(0.35, 1.0, 7))
-    steps = al.step_counts(v, 100, 4, 0.8, 0.3)
+    steps = al.step_counts(v, 100, 4, 0.8, 0.25)
     sh = al.patch_shares(v, steps)
     r = [vi / m / s for vi, m, s in zip(v, steps, sh) if m]
     assert np.allclose(r, r[0]) and abs(sum(sh) - 1) < 1e-12

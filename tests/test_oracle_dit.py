@@ -303,3 +303,30 @@ def test_guidance_and_update_composition(tiny):
     g = e[1] + 1.5 * (e[0] - e[1])
     A, Bc, C = schedule.ddim_coefficients(schedule.alpha_bar(), 750, 500)
     np.testing.assert_allclose(r["x_out"], A * x[:, :8] - Bc * g, rtol=1e-14, atol=1e-14)
+
+
+def _branch_order_holds(hdr, params, x, labels, step=dit.patch_step):
+    """Guidance at g = 0 is the null-label model alone, at g = 1 the
+    class-label model alone (eps_u + g (eps_c - eps_u) with eps_c from the
+    class label and eps_u from the null label): checked against single-branch
+    runs of the denoiser, which involve no guidance at all."""
+    cls, null = int(labels[0]), int(labels[1])
+    R = hdr["grid"]
+    ok = True
+    for g, lab in ((0.0, null), (1.0, cls)):
+        two = step(hdr, params, x, 0, R, 500, 250, [cls, null], g)
+        one = step(hdr, params, x, 0, R, 500, 250, [lab], 7.0)   # g unused for one branch
+        ok &= bool(np.allclose(two["eps_guided"], one["eps_guided"], rtol=1e-12, atol=1e-13))
+        ok &= bool(np.allclose(two["x_out"], one["x_out"], rtol=1e-12, atol=1e-13))
+    return ok
+
+
+def test_guidance_branch_order_from_single_branch_runs(tiny):
+    cfg, hdr, params, x, labels = tiny
+    assert labels[1] == cfg.num_classes and labels[0] != labels[1]
+    assert _branch_order_holds(hdr, params, x, labels)
+    # and the two single-branch runs differ, so the pin has teeth
+    R = cfg.R
+    a = dit.patch_step(hdr, params, x, 0, R, 500, 250, [int(labels[0])], 1.0)["eps_guided"]
+    b = dit.patch_step(hdr, params, x, 0, R, 500, 250, [int(labels[1])], 1.0)["eps_guided"]
+    assert dit.rel_l2(a, b) > 1e-3

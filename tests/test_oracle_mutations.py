@@ -124,3 +124,17 @@ def test_mutation_scheduler_sign(monkeypatch):
     bad = A * x + Bc * eps
     assert abs(good - (a_p * x0 + s_p * eps)) < 1e-12
     assert abs(bad - (a_p * x0 + s_p * eps)) > 1e-3
+
+
+def test_mutation_guidance_branch_swap(model, monkeypatch):
+    """eps_c + g (eps_u - eps_c) (branches swapped) breaks the single-branch pin."""
+    from tests.test_oracle_dit import _branch_order_holds
+    hdr, params, x, labels = model
+    assert _branch_order_holds(hdr, params, x, labels)
+
+    def swapped(eps, cfg_scale):
+        if eps.shape[0] == 1:
+            return eps[0]
+        return eps[0] + cfg_scale * (eps[1] - eps[0])
+    monkeypatch.setattr(dit, "guided_eps", swapped)
+    assert not _branch_order_holds(hdr, params, x, labels)
