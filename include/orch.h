@@ -75,7 +75,14 @@ int orch_load_dit_weights(orch_ctx* ctx, const void* host_blob, size_t nbytes);
  * elements, N_kv = (latent/patch)^2.  Layout per (block l, branch b), at
  * element offset (l * cfg_batch + b) * 2 * N_kv * hidden: K as
  * [heads][N_kv][head_dim], then V transposed as [heads][head_dim][N_kv].
- * Token index n = row * (latent/patch) + column. */
+ * Token index n = row * (latent/patch) + column.
+ * Why not token-major [N_kv][hidden] for K and V: the attention kernel reads
+ * a tile of 64 consecutive keys of one head; head-major K makes that tile one
+ * contiguous run, and V^T makes its values contiguous 128-byte runs per
+ * channel, the row layout of the PV product's MFMA operand.  A band of token
+ * rows is still a set of contiguous runs (one per head for K, one per head
+ * and channel for V^T), so the refresh and a transfer of a band to a peer
+ * need no packing. */
 size_t orch_stale_kv_bytes(const orch_ctx* ctx);
 
 /* One executed denoising step of one device (Algorithm 1; §I update with
@@ -100,8 +107,12 @@ size_t orch_stale_kv_bytes(const orch_ctx* ctx);
  *   out_eps     device fp32 [cfg_batch][out_ch][2r][latent] or NULL: the
  *               unguided eps of every branch for the band (r = row_end -
  *               row_begin, 2r = r * patch latent rows).
- *   out_x_patch device fp32 [in_ch][r*patch][latent]: the band of x_{t_prev}.
- *               Must not overlap x_full, stale_kv or out_eps.
+ *   out_x_patch device fp32: the band of x_{t_prev}.  Either a separate
+ *               [in_ch][r*patch][latent] array, or exactly the band of x_full
+ *               (x_full + row_begin*patch*latent): the band is then updated
+ *               in place, in x_full's layout (channel stride latent*latent;
+ *               the step reads x_full before it writes the band).  Any other
+ *               overlap with x_full, stale_kv or out_eps is an error.
  * Errors: ORCH_EINVAL for a bad band, timestep, label, NULL pointer or
  * overlap; ORCH_ENOWEIGHTS before weights are loaded; ORCH_EHIP. */
 int orch_patch_denoise_step(orch_ctx* ctx, const float* x_full, int row_begin, int row_end,
@@ -142,7 +153,10 @@ int orch_sample_patch_parallel(orch_ctx* ctx, float* latent, int n_bands, const 
 /* The fused guidance + scheduler update of §I, elementwise over n floats:
  *   eps = eps_uncond ? eps_uncond + g (eps_cond - eps_uncond) : eps_cond
  *   out = a x - b eps + c z          (z may be NULL when c == 0)
- * All pointers are device fp32 arrays of n elements; out may equal x. */
+ * All pointers are device fp32 arrays of n elements; out may equal x.
+ * With eps_uncond == NULL this is the plain update of one eps; the two-eps
+ * form fuses classifier-free guidance into the same pass over memory (no
+ * separate guided-eps array is written and read back). */
 int orch_scheduler_update(const float* x, const float* eps_cond, const float* eps_uncond,
                           float cfg_scale, const float* z, double a, double b, double c,
                           float* out, size_t n, void* hip_stream);
@@ -186,6 +200,16 @@ enum {
   ORCH_KCLASS_FC2, ORCH_KCLASS_FINAL, ORCH_KCLASS_UPDATE, ORCH_KCLASS_COUNT
 };
 int orch_set_kernel_timing(orch_ctx* ctx, int enable);
+
+/* Work split of the step's kernels (default on).  On: GEMMs with too few
+ * output tiles to fill the GPU split K over more workgroups, and attention
+ * cuts query tiles between workgroups, whenever the context's workspace
+ * allows (faster for short bands; the summation order then depends on the
+ * band's height).  Off: every GEMM runs unsplit and every attention query
+ * tile stays in one workgroup, so each output's summation order is fixed by
+ * the token alone: bands stitched from a buffer holding the full step's K/V
+ * reproduce the all-rows step bit for bit.  Takes effect at the next step. */
+int orch_set_work_split(orch_ctx* ctx, int enable);
 int orch_kernel_times(orch_ctx* ctx, double* total_ms, long long* launches);
 
 /* ---- kernel-level entry points ------------------------------------------

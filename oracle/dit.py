@@ -214,7 +214,8 @@ def assemble_kv(stale, k, v, tok0: int):
 
 def denoiser_band(hdr, params, x_full, row_begin: int, row_end: int, t: int,
                   labels: Sequence[int], stale_kv=None, dtype=np.float64,
-                  keep_kv: bool = False, keep_h: bool = False):
+                  keep_kv: bool = False, keep_h: bool = False,
+                  out_rows: Optional[Sequence[int]] = None):
     """eps_theta for the band's tokens, every guidance branch.
 
     Returns dict with
@@ -223,6 +224,13 @@ def denoiser_band(hdr, params, x_full, row_begin: int, row_end: int, t: int,
               band's fresh (K, V), token-major [N_q, H],
       h       (if keep_h) residual stream after patch embedding and after
               every block, list of [B, N_q, H].
+
+    out_rows (optional): band-relative token rows whose outputs are wanted.
+    After the last block's QKV projection every token's output depends only
+    on its own residual row and on the keys/values, so the last block's
+    attention, MLP and the final layer are then evaluated for those rows'
+    tokens only (its keys/values still come from every band token); eps
+    covers those rows, in the order given: [B, C_out, len(out_rows)*p, W].
     """
     H, heads, L, R = hdr["hidden"], hdr["heads"], hdr["n_blocks"], hdr["grid"]
     B = len(labels)
@@ -232,6 +240,11 @@ def denoiser_band(hdr, params, x_full, row_begin: int, row_end: int, t: int,
     full = row_begin == 0 and row_end == R
     if stale_kv is None and not full:
         raise ValueError("a band of fewer than all rows needs the stale buffer")
+    sel = None
+    if out_rows is not None:
+        if any(r < 0 or r >= n_rows for r in out_rows):
+            raise ValueError("out_rows must be band-relative rows")
+        sel = np.concatenate([np.arange(r * R, (r + 1) * R) for r in out_rows])
 
     c = conditioning(hdr, params, t, labels, dtype)
     blocks, (fshift, fscale) = adaln_vectors(hdr, params, c)
@@ -243,7 +256,9 @@ def denoiser_band(hdr, params, x_full, row_begin: int, row_end: int, t: int,
     for l in range(L):
         pre = f"blocks.{l}."
         s1, c1, g1, s2, c2, g2 = blocks[l]
+        restrict = sel is not None and l == L - 1
         layer_kv = []
+        new_h = []
         for b in range(B):
             u = modulate(layer_norm(h[b]), s1[b], c1[b])
             qkv = linear(u, params[pre + "qkv.weight"], params[pre + "qkv.bias"])
@@ -252,20 +267,26 @@ def denoiser_band(hdr, params, x_full, row_begin: int, row_end: int, t: int,
                 K, V = k, v
             else:
                 K, V = assemble_kv(stale_kv_block(hdr, stale_kv, B, l, b, dtype), k, v, tok0)
+            hb = h[b]
+            if restrict:                      # only the wanted tokens leave the last block
+                q, hb = q[sel], hb[sel]
             o = attention(q, K, V, heads)
-            h[b] = h[b] + g1[b] * linear(o, params[pre + "proj.weight"], params[pre + "proj.bias"])
-            u2 = modulate(layer_norm(h[b]), s2[b], c2[b])
+            hb = hb + g1[b] * linear(o, params[pre + "proj.weight"], params[pre + "proj.bias"])
+            u2 = modulate(layer_norm(hb), s2[b], c2[b])
             m = gelu_tanh(linear(u2, params[pre + "fc1.weight"], params[pre + "fc1.bias"]))
-            h[b] = h[b] + g2[b] * linear(m, params[pre + "fc2.weight"], params[pre + "fc2.bias"])
+            hb = hb + g2[b] * linear(m, params[pre + "fc2.weight"], params[pre + "fc2.bias"])
+            new_h.append(hb)
             if keep_kv:
                 layer_kv.append((k, v))
+        h = np.stack(new_h)
         if keep_kv:
             kv_keep.append(layer_kv)
         if keep_h:
             h_keep.append(h.copy())
 
+    n_out = n_rows if sel is None else len(out_rows)
     eps = np.stack([unpatchify_rows(hdr, final_layer(hdr, params, h[b], fshift[b], fscale[b]),
-                                    n_rows) for b in range(B)])
+                                    n_out) for b in range(B)])
     out = {"eps": eps}
     if keep_kv:
         out["kv"] = kv_keep
@@ -285,15 +306,18 @@ def guided_eps(eps, cfg_scale: float):
 def patch_step(hdr, params, x_full, row_begin: int, row_end: int, t: int, t_prev: int,
                labels: Sequence[int], cfg_scale: float, stale_kv=None, eta: float = 0.0,
                z=None, T: int = 1000, beta_start: float = 1e-4, beta_end: float = 2e-2,
-               dtype=np.float64, keep_kv: bool = False, keep_h: bool = False) -> Dict:
+               dtype=np.float64, keep_kv: bool = False, keep_h: bool = False,
+               out_rows: Optional[Sequence[int]] = None) -> Dict:
     """One executed step of one device: eps for the band, guidance, and the
-    scheduler update of the band rows (x_out = A x - Bc eps + C z)."""
+    scheduler update of the band rows (x_out = A x - Bc eps + C z).  With
+    out_rows, eps and x_out cover only those band-relative token rows."""
     res = denoiser_band(hdr, params, x_full, row_begin, row_end, t, labels, stale_kv,
-                        dtype, keep_kv, keep_h)
+                        dtype, keep_kv, keep_h, out_rows)
     ab = schedule.alpha_bar(T, beta_start, beta_end)
     A, Bc, C = schedule.ddim_coefficients(ab, t, t_prev, eta)
     p = hdr["patch"]
-    rows = slice(row_begin * p, row_end * p)
+    band = range(row_end - row_begin) if out_rows is None else out_rows
+    rows = [(row_begin + r) * p + dy for r in band for dy in range(p)]
     x_band = np.asarray(x_full, dtype=np.float64)[:, rows, :]
     z_band = None if z is None else np.asarray(z, dtype=np.float64)[:, rows, :]
     g = guided_eps(res["eps"].astype(np.float64), cfg_scale)

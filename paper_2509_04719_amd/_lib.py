@@ -25,7 +25,7 @@ SYMBOLS = (
     "orch_op_attention", "orch_op_conditioning", "orch_op_patch_embed", "orch_op_final_layer",
     "orch_attention_workspace_bytes", "orch_set_kernel_timing", "orch_kernel_times",
     "orch_linear_workspace_bytes",
-    "orch_plan_devices", "orch_sample_patch_parallel",
+    "orch_plan_devices", "orch_sample_patch_parallel", "orch_set_work_split",
 )
 KCLASSES = ("conditioning", "patch_embed", "layernorm", "qkv_gemm", "attention", "proj_gemm",
             "fc1_gemm", "fc2_gemm", "final_layer", "update")
@@ -75,6 +75,7 @@ def _load():
         "orch_op_attention": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, vp, sz, i, vp]),
         "orch_attention_workspace_bytes": (sz, [i, i, i, i, i, i]),
         "orch_set_kernel_timing": (i, [vp, i]),
+        "orch_set_work_split": (i, [vp, i]),
         "orch_kernel_times": (i, [vp, C.POINTER(d), C.POINTER(C.c_longlong)]),
         "orch_op_conditioning": (i, [vp, i, C.POINTER(i), vp, vp]),
         "orch_op_patch_embed": (i, [vp, vp, i, i, vp, vp]),
@@ -178,6 +179,9 @@ class DiTStep:
         check(lib.orch_sample_patch_parallel(self.handle, _ptr(latent), n, sp, tr, tg,
                                              len(t_grid) - 1, int(warmup), lab, float(cfg_scale),
                                              _ptr(kv_a), _ptr(kv_b), _stream(stream)))
+
+    def set_work_split(self, enable: bool):
+        check(lib.orch_set_work_split(self.handle, int(enable)))
 
     def set_kernel_timing(self, enable: bool):
         check(lib.orch_set_kernel_timing(self.handle, int(enable)))

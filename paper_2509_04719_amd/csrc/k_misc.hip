@@ -382,12 +382,14 @@ hipError_t launch_final_linear(const FinalParams& p, int dtype, hipStream_t s) {
 
 // ---------------------------------------------------------------------------
 // Guidance + scheduler update: out = a x - b (eu + g (ec - eu)) + c z.
-__global__ __launch_bounds__(256) void update_vec4_kernel(const float* __restrict__ x, int ldx,
+// out may be x itself (each element is read before it is written, by the
+// same thread), so neither carries __restrict__.
+__global__ __launch_bounds__(256) void update_vec4_kernel(const float* x, int ldx,
                                                           const float* __restrict__ ec,
                                                           const float* __restrict__ eu, float g,
                                                           const float* __restrict__ z, int ldz,
                                                           float a, float b, float c,
-                                                          float* __restrict__ out, int ldo,
+                                                          float* out, int ldo,
                                                           int rows, size_t cols4) {
   const size_t total = (size_t)rows * cols4;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < total;
@@ -419,12 +421,12 @@ __global__ __launch_bounds__(256) void update_vec4_kernel(const float* __restric
   }
 }
 
-__global__ __launch_bounds__(256) void update_scalar_kernel(const float* __restrict__ x, int ldx,
+__global__ __launch_bounds__(256) void update_scalar_kernel(const float* x, int ldx,
                                                             const float* __restrict__ ec,
                                                             const float* __restrict__ eu, float g,
                                                             const float* __restrict__ z, int ldz,
                                                             float a, float b, float c,
-                                                            float* __restrict__ out, int ldo,
+                                                            float* out, int ldo,
                                                             int rows, size_t cols) {
   const size_t total = (size_t)rows * cols;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < total;

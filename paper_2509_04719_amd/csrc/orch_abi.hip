@@ -96,6 +96,7 @@ struct orch_ctx {
   float* gemm_ws = nullptr;   // k-split partials of short (small-band) GEMMs
   size_t gemm_ws_elems = 0;
   float* lat[3] = {};   // latents of the patch-parallel sampler
+  bool work_split = true;   // k-split of short GEMMs, cut attention query tiles
 
   // per-kernel timing: event pairs recorded around each launch of a step
   struct Timing {
@@ -567,6 +568,8 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
   const size_t es = esize(dt);
   const int H = x->H, F = x->F, B = x->B;
   const int M = B * n_tok;
+  float* gemm_ws = x->work_split ? x->gemm_ws : nullptr;
+  void* attn_ws = x->work_split ? x->attn_ws : nullptr;
 
   rc = run_conditioning(x, t, labels, x->mod, s);
   if (rc) return rc;
@@ -593,7 +596,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
     EpiParams eq{};
     eq.q_scale = q_scaled ? 1.4426950408889634f / sqrtf((float)x->d) : 1.0f;
     eq.bias = x->b_qkv[l];
-    eq.ws = x->gemm_ws; eq.ws_elems = x->gemm_ws_elems;
+    eq.ws = gemm_ws; eq.ws_elems = x->gemm_ws_elems;
     eq.rows_per_batch = n_tok;
     eq.q = x->q;
     eq.heads = x->heads; eq.hidden = H; eq.head_dim = x->d;
@@ -621,7 +624,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
     }
     ap.B = B; ap.heads = x->heads; ap.n_q = n_tok; ap.n_kv = x->n_kv; ap.d = x->d; ap.out = x->att;
     ap.q_scaled = q_scaled;
-    ap.ws = x->attn_ws; ap.ws_bytes = x->attn_ws_bytes;
+    ap.ws = attn_ws; ap.ws_bytes = x->attn_ws_bytes;
     {
       KernelTimer kt(x, ORCH_KCLASS_ATTENTION, s);
       HIP_TRY(launch_attention(ap, dt, s), "attention launch");
@@ -630,7 +633,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
     EpiParams eo{};
     eo.out = x->h; eo.bias = x->b_proj[l]; eo.gate = mb + 2 * H; eo.gate_stride = x->n_mod;
     eo.rows_per_batch = n_tok;
-    eo.ws = x->gemm_ws; eo.ws_elems = x->gemm_ws_elems;
+    eo.ws = gemm_ws; eo.ws_elems = x->gemm_ws_elems;
     {
       KernelTimer kt(x, ORCH_KCLASS_PROJ, s);
       HIP_TRY(launch_gemm(x->att, x->w_proj[l], M, H, H, kEpiResidual, eo, dt, s), "proj launch");
@@ -643,7 +646,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
 
     EpiParams e1{};
     e1.out = x->mlp; e1.bias = x->b_fc1[l];
-    e1.ws = x->gemm_ws; e1.ws_elems = x->gemm_ws_elems;
+    e1.ws = gemm_ws; e1.ws_elems = x->gemm_ws_elems;
     {
       KernelTimer kt(x, ORCH_KCLASS_FC1, s);
       HIP_TRY(launch_gemm(x->u, x->w_fc1[l], M, F, H, kEpiGelu, e1, dt, s), "fc1 launch");
@@ -652,7 +655,7 @@ int run_step(orch_ctx* x, const float* x_full, int rb, int re, int t, int t_prev
     EpiParams e2{};
     e2.out = x->h; e2.bias = x->b_fc2[l]; e2.gate = mb + 5 * H; e2.gate_stride = x->n_mod;
     e2.rows_per_batch = n_tok;
-    e2.ws = x->gemm_ws; e2.ws_elems = x->gemm_ws_elems;
+    e2.ws = gemm_ws; e2.ws_elems = x->gemm_ws_elems;
     {
       KernelTimer kt(x, ORCH_KCLASS_FC2, s);
       HIP_TRY(launch_gemm(x->mlp, x->w_fc2[l], M, H, F, kEpiResidual, e2, dt, s), "fc2 launch");
@@ -703,12 +706,17 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
   const size_t out_bytes = (size_t)c.in_ch * n_rows * p * c.latent * 4;
   const size_t eps_bytes = (size_t)x->B * c.out_ch * n_rows * p * c.latent * 4;
   const size_t kv_bytes = orch_stale_kv_bytes(x);
-  if (ranges_overlap(out_x_patch, out_bytes, x_full, x_bytes) ||
-      ranges_overlap(out_x_patch, out_bytes, stale_kv, kv_bytes) ||
-      ranges_overlap(out_x_patch, out_bytes, out_eps, eps_bytes) ||
+  // out_x_patch may be the band of x_full itself: the band is then updated in
+  // place, in x_full's layout (channel stride latent * latent); any other
+  // overlap with an input is an error
+  const bool in_place = out_x_patch == x_full + (size_t)rb * p * c.latent;
+  const size_t out_span = in_place ? x_bytes - (size_t)rb * p * c.latent * 4 : out_bytes;
+  if ((!in_place && ranges_overlap(out_x_patch, out_bytes, x_full, x_bytes)) ||
+      ranges_overlap(out_x_patch, out_span, stale_kv, kv_bytes) ||
+      ranges_overlap(out_x_patch, out_span, out_eps, eps_bytes) ||
       ranges_overlap(out_eps, eps_bytes, x_full, x_bytes) ||
       ranges_overlap(out_eps, eps_bytes, stale_kv, kv_bytes))
-    return fail(ORCH_EINVAL, "output buffers overlap inputs");
+    return fail(ORCH_EINVAL, "output buffers overlap inputs (out_x_patch may only be exactly the band of x_full)");
   if (((uintptr_t)x_full | (uintptr_t)stale_kv | (uintptr_t)out_x_patch | (uintptr_t)out_eps |
        (uintptr_t)z) & 15)
     return fail(ORCH_EINVAL, "device buffers must be 16-byte aligned");
@@ -717,7 +725,7 @@ int orch_patch_denoise_step(orch_ctx* x, const float* x_full, int rb, int re, in
 
   return run_step(x, x_full, rb, re, t, t_prev, labels, cfg_scale, stale_kv,
                   refresh ? stale_kv : nullptr, z, eta, out_eps, out_x_patch,
-                  n_rows * p * c.latent, (hipStream_t)hip_stream);
+                  in_place ? (int)lat2 : n_rows * p * c.latent, (hipStream_t)hip_stream);
 }
 
 int orch_sample_patch_parallel(orch_ctx* x, float* latent, int n_bands, const int* row_splits,
@@ -885,10 +893,15 @@ size_t orch_attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int h
   return attention_workspace_bytes(B, heads, n_q, n_kv, head_dim, dtype);
 }
 
-int orch_op_attention(const void* q, const void* kv_stale, size_t stale_bs, const void* kv_fresh,
-                      size_t fresh_bs, int fresh_begin, int n_fresh, int B, int heads, int n_q,
-                      int n_kv, int head_dim, void* out, void* workspace, size_t workspace_bytes,
-                      int dtype, void* hip_stream) {
+}  // extern "C"
+
+namespace orch_detail {
+
+// Shape and pointer checks shared by the attention entry points.
+int check_attention_args(const void* q, const void* kv_stale, size_t stale_bs,
+                         const void* kv_fresh, size_t fresh_bs, int fresh_begin, int n_fresh,
+                         int B, int heads, int n_q, int n_kv, int head_dim, const void* out,
+                         int dtype) {
   if (!q || !kv_stale || !out || (n_fresh > 0 && !kv_fresh)) return fail(ORCH_EINVAL, "NULL pointer");
   if (B < 1 || heads < 1 || n_q < 0 || n_kv < 1 || n_fresh < 0 || fresh_begin < 0 ||
       fresh_begin + n_fresh > n_kv)
@@ -900,12 +913,35 @@ int orch_op_attention(const void* q, const void* kv_stale, size_t stale_bs, cons
   if (stale_bs < 2 * (size_t)n_kv * H || (n_fresh > 0 && fresh_bs < 2 * (size_t)n_fresh * H))
     return fail(ORCH_EINVAL, "branch stride too small");
   if (dtype != ORCH_F32 && dtype != ORCH_BF16) return fail(ORCH_EINVAL, "bad dtype");
+  return ORCH_OK;
+}
+
+AttnParams attention_params(const void* q, const void* kv_stale, size_t stale_bs,
+                            const void* kv_fresh, size_t fresh_bs, int fresh_begin, int n_fresh,
+                            int B, int heads, int n_q, int n_kv, int head_dim, void* out) {
   AttnParams ap{};
   ap.q = q; ap.kv_stale = kv_stale; ap.stale_bs = stale_bs; ap.kv_fresh = kv_fresh;
   ap.fresh_bs = fresh_bs; ap.fresh_begin = fresh_begin; ap.n_fresh = n_fresh; ap.B = B;
   ap.heads = heads; ap.n_q = n_q; ap.n_kv = n_kv; ap.d = head_dim; ap.out = out;
-  ap.ws = workspace; ap.ws_bytes = workspace ? workspace_bytes : 0;
   ap.fresh_n = n_fresh; ap.fresh_off = 0;
+  return ap;
+}
+
+}  // namespace orch_detail
+
+extern "C" {
+
+int orch_op_attention(const void* q, const void* kv_stale, size_t stale_bs, const void* kv_fresh,
+                      size_t fresh_bs, int fresh_begin, int n_fresh, int B, int heads, int n_q,
+                      int n_kv, int head_dim, void* out, void* workspace, size_t workspace_bytes,
+                      int dtype, void* hip_stream) {
+  int rc = orch_detail::check_attention_args(q, kv_stale, stale_bs, kv_fresh, fresh_bs,
+                                             fresh_begin, n_fresh, B, heads, n_q, n_kv, head_dim,
+                                             out, dtype);
+  if (rc) return rc;
+  AttnParams ap = orch_detail::attention_params(q, kv_stale, stale_bs, kv_fresh, fresh_bs, fresh_begin,
+                                   n_fresh, B, heads, n_q, n_kv, head_dim, out);
+  ap.ws = workspace; ap.ws_bytes = workspace ? workspace_bytes : 0;
   HIP_TRY(launch_attention(ap, dtype, (hipStream_t)hip_stream), "attention launch");
   return ORCH_OK;
 }
@@ -938,6 +974,12 @@ int orch_op_final_layer(orch_ctx* x, const float* h, int rb, int re, const float
   int rc = check_device(x);
   if (rc) return rc;
   return run_final(x, h, rb, re, mod, out_eps, (hipStream_t)hip_stream);
+}
+
+int orch_set_work_split(orch_ctx* x, int enable) {
+  if (!x) return fail(ORCH_EINVAL, "ctx is NULL");
+  x->work_split = enable != 0;
+  return ORCH_OK;
 }
 
 int orch_set_kernel_timing(orch_ctx* x, int enable) {

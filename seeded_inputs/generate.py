@@ -174,6 +174,14 @@ def make_labels(cfg: DiTConfig, seed: int = 0) -> np.ndarray:
     return np.array([lab, cfg.num_classes], dtype=np.int32)
 
 
+def make_stale_latent(cfg: DiTConfig, seed: int = 0) -> np.ndarray:
+    """float32 [in_ch, latent, latent] ~ N(0, 1), independent of make_latent:
+    the sample a model-consistent stale buffer is computed from (its K/V
+    under a full-image step), drawn from the stale-buffer stream."""
+    rng = np.random.default_rng([seed, STREAM_STALE, 1])
+    return rng.standard_normal((cfg.in_ch, cfg.latent, cfg.latent)).astype(np.float32)
+
+
 def stale_kv_elems(cfg: DiTConfig) -> int:
     return cfg.n_blocks * cfg.cfg_batch * 2 * cfg.n_kv * cfg.hidden
 

@@ -60,7 +60,10 @@ def test_null_and_overlap(orch_lib, setup):
     assert _step(orch_lib, ctx, None, kv, out) == orch_lib.ORCH_EINVAL
     assert _step(orch_lib, ctx, x, None, out) == orch_lib.ORCH_EINVAL
     assert _step(orch_lib, ctx, x, kv, None) == orch_lib.ORCH_EINVAL
-    assert _step(orch_lib, ctx, x, kv, x) == orch_lib.ORCH_EINVAL          # out inside x_full
+    # inside x_full but not exactly its band
+    assert _step(orch_lib, ctx, x, kv, x.view(-1)[4:]) == orch_lib.ORCH_EINVAL
+    assert "overlap" in orch_lib.last_error()
+    assert _step(orch_lib, ctx, x, kv, x.view(-1)[CFG.latent * 2:], rb=0) == orch_lib.ORCH_EINVAL
     assert "overlap" in orch_lib.last_error()
     assert _step(orch_lib, ctx, x, kv, kv) == orch_lib.ORCH_EINVAL
     ok = _step(orch_lib, ctx, x, kv, out)
@@ -124,3 +127,22 @@ def test_kernel_timing_counts(orch_lib, setup):
     torch.cuda.synchronize()
     assert torch.equal(out0, out1)
     assert all(v == (0.0, 0) for v in ctx.kernel_times().values())
+
+
+@pytest.mark.parametrize("rb,re", [(0, 4), (3, 8), (2, 5)])
+def test_in_place_band_update(orch_lib, setup, rb, re):
+    """out_x_patch == the band of x_full: the band is updated in place (in
+    x_full's layout), bitwise as the separate output, other rows untouched."""
+    ctx, _, x, kv = setup
+    p = CFG.patch
+    out = empty((CFG.in_ch, (re - rb) * p, CFG.latent))
+    assert _step(orch_lib, ctx, x, kv, out, rb=rb, re=re) == orch_lib.ORCH_OK
+    xi = x.clone()
+    band = xi[:, rb * p:re * p]                     # a view starting at the band of xi
+    assert band.data_ptr() == xi.data_ptr() + rb * p * CFG.latent * 4
+    assert _step(orch_lib, ctx, xi, kv, band, rb=rb, re=re) == orch_lib.ORCH_OK, \
+        orch_lib.last_error()
+    torch.cuda.synchronize()
+    assert torch.equal(xi[:, rb * p:re * p], out)
+    assert torch.equal(xi[:, :rb * p], x[:, :rb * p])
+    assert torch.equal(xi[:, re * p:], x[:, re * p:])

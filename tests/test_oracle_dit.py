@@ -330,3 +330,20 @@ def test_guidance_branch_order_from_single_branch_runs(tiny):
     a = dit.patch_step(hdr, params, x, 0, R, 500, 250, [int(labels[0])], 1.0)["eps_guided"]
     b = dit.patch_step(hdr, params, x, 0, R, 500, 250, [int(labels[1])], 1.0)["eps_guided"]
     assert dit.rel_l2(a, b) > 1e-3
+
+
+def test_sampled_output_rows_equal_the_whole_band(tiny):
+    """out_rows restricts the last block and the final layer to some token
+    rows; every output row is the same as in the whole-band evaluation."""
+    cfg, hdr, params, x, labels = tiny
+    stale = generate.make_stale_kv(cfg, 0)
+    rb, re = 1, 7
+    whole = dit.patch_step(hdr, params, x, rb, re, 750, 500, labels, 1.5, stale)
+    rows = [4, 0, 5]
+    part = dit.patch_step(hdr, params, x, rb, re, 750, 500, labels, 1.5, stale, out_rows=rows)
+    p = cfg.patch
+    lat = [r * p + dy for r in rows for dy in range(p)]
+    np.testing.assert_allclose(part["eps"], whole["eps"][:, :, lat], rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(part["x_out"], whole["x_out"][:, lat], rtol=1e-13, atol=1e-14)
+    with pytest.raises(ValueError):
+        dit.patch_step(hdr, params, x, rb, re, 750, 500, labels, 1.5, stale, out_rows=[6])
