@@ -274,6 +274,21 @@ int orch_op_attention(const void* q, const void* kv_stale, size_t stale_branch_s
 size_t orch_attention_workspace_bytes(int B, int heads, int n_q, int n_kv, int head_dim,
                                       int dtype);
 
+/* orch_op_attention for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments without the workspace, the same kernels
+ * and work plan (query tiles cut between workgroups where that pays).  The
+ * cut tiles' parts go to a static device array of 20 MiB per GPU, held until
+ * the process ends, which covers every shape of the work plan (at most 512
+ * workgroups, head_dim <= 72); a shape needing more returns ORCH_EINVAL.
+ * Calls nothing that allocates.  Every call on one GPU shares that GPU's
+ * array: calls that overlap on one GPU (concurrent streams or threads) race.
+ * Errors as orch_op_attention. */
+int orch_op_attention_noalloc(const void* q, const void* kv_stale, size_t stale_branch_stride,
+                              const void* kv_fresh, size_t fresh_branch_stride, int fresh_begin,
+                              int n_fresh, int B, int heads, int n_q, int n_kv, int head_dim,
+                              void* out, int dtype, void* hip_stream);
+
 /* Conditioning of the loaded model: out fp32 [cfg_batch][6*H*n_blocks + 2*H],
  * the adaLN vectors of every block followed by the final layer's
  * (shift, scale), for timestep t and host labels[cfg_batch]. */

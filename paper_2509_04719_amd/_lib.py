@@ -26,6 +26,7 @@ SYMBOLS = (
     "orch_attention_workspace_bytes", "orch_set_kernel_timing", "orch_kernel_times",
     "orch_linear_workspace_bytes",
     "orch_plan_devices", "orch_sample_patch_parallel", "orch_set_work_split",
+    "orch_op_attention_noalloc",
 )
 KCLASSES = ("conditioning", "patch_embed", "layernorm", "qkv_gemm", "attention", "proj_gemm",
             "fc1_gemm", "fc2_gemm", "final_layer", "update")
@@ -74,6 +75,7 @@ def _load():
         "orch_op_qkv_projection": (i, [vp, i, i, i, vp, vp, i, i, vp, vp, sz, i, i, i, vp]),
         "orch_op_attention": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, vp, sz, i, vp]),
         "orch_attention_workspace_bytes": (sz, [i, i, i, i, i, i]),
+        "orch_op_attention_noalloc": (i, [vp, vp, sz, vp, sz, i, i, i, i, i, i, i, vp, i, vp]),
         "orch_set_kernel_timing": (i, [vp, i]),
         "orch_set_work_split": (i, [vp, i]),
         "orch_kernel_times": (i, [vp, C.POINTER(d), C.POINTER(C.c_longlong)]),
