@@ -35,6 +35,10 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 METRIC = "patch-step ms and TFLOP/s vs bf16 MFMA peak, DiT-XL/2 1024px, 1 GPU"
+SWEEP_SHARES = (0.10, 0.25, 0.40, 0.65, 1.00)   # elastic band shares of the 1024px grid
+CPU_SHARE = 0.10                                 # band the oracle is timed on, whole step
+PROFILE_ROWS = (4, 8, 16, 32, 64)                # band heights of a device's time profile
+MFMA_KERNELS = ("qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm")
 
 # HBM traffic of the dominant kernel, from two rocprofv3 --pmc runs of
 # `bench.py --pmc-probe` (FETCH_SIZE, then WRITE_SIZE) turned into a report by
@@ -99,7 +103,10 @@ def pmc_probe(a) -> int:
     ctx = L.DiTStep(cfg, generate.make_weight_blob(cfg, 0))
     x = torch.from_numpy(generate.make_latent(cfg, 0)).to(dev)
     labels = generate.make_labels(cfg, 0)
-    kv = torch.from_numpy(generate.make_stale_kv(cfg, 0).view(np.int16)).to(dev).view(torch.bfloat16)
+    kv = torch.zeros(ctx.stale_kv_bytes() // 2, dtype=torch.bfloat16, device=dev)
+    xs = torch.from_numpy(generate.make_stale_latent(cfg, 0)).to(dev)
+    full_out = torch.empty((cfg.in_ch, cfg.latent, cfg.latent), device=dev)
+    ctx.step(xs, 0, cfg.R, t + cfg.T // cfg.steps, t, labels, cfg.cfg_scale, kv, 1, full_out)
     out = torch.empty((cfg.in_ch, rows * cfg.patch, cfg.latent), device=dev)
     for _ in range(5):
         ctx.step(x, 0, rows, t, tp, labels, cfg.cfg_scale, kv, 1, out)
@@ -294,35 +301,52 @@ def step_kernel_split(ctx, cfg, n_q: int, run_step, steps: int):
     return out
 
 
-def cpu_baseline(cfg, blob, x, labels, stale, rb, re, t, tp, blocks: int):
-    """The oracle (float64 numpy) on the same band, truncated to `blocks`
-    DiT blocks; rate scaled to the metric's unit by the sample's FLOPs."""
-    import dataclasses
+def host_info() -> dict:
+    """CPU model, numpy and its BLAS, and the cores this process may use."""
+    import platform
 
+    import numpy as np
+    model = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas, threads = "unknown", None
+    try:
+        from threadpoolctl import threadpool_info
+        infos = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if infos:
+            blas = f"{infos[0].get('internal_api')} {infos[0].get('version')}"
+            threads = infos[0].get("num_threads")
+    except Exception:
+        pass
+    return {"cpu_model": model, "numpy": np.__version__, "blas": blas, "blas_threads": threads,
+            "affinity_cores": len(os.sched_getaffinity(0))}
+
+
+def cpu_baseline(cfg, blob, x, labels, stale, rb, re, t, tp):
+    """The oracle (float64 numpy) timed on one whole band step: every block,
+    both guidance branches, the update; no extrapolation."""
     import numpy as np
 
     from oracle import blob as oblob
     from oracle import dit
     hdr, params = oblob.read_blob(blob, np.float64)
-    hdr = dict(hdr, n_blocks=blocks)
     t0 = time.perf_counter()
     dit.patch_step(hdr, params, x, rb, re, t, tp, labels, cfg.cfg_scale, stale)
     dt = time.perf_counter() - t0
-    small = dataclasses.replace(cfg, n_blocks=blocks)
-    fl = step_flops(small, (re - rb) * cfg.R)
-    threads = None
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads") or 0) for i in threadpool_info()) or None
-    except Exception:
-        pass
-    if threads is None:
-        threads = len(os.sched_getaffinity(0))
-    return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{cfg.name} band rows [{rb},{re}), both guidance branches, first {blocks} of "
-                      f"{cfg.n_blocks} blocks, float64 numpy; {fl / 1e12:.3f} TFLOP in {dt:.1f} s",
-            "ms_per_full_step_extrapolated": round(step_flops(cfg, (re - rb) * cfg.R) / (fl / dt) * 1e3, 1)}
+    fl = step_flops(cfg, (re - rb) * cfg.R)
+    info = host_info()
+    cores = info["blas_threads"] or info["affinity_cores"]
+    return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{cfg.name} band rows [{rb},{re}) ({re - rb}/{cfg.R}), all {cfg.n_blocks} "
+                      f"blocks, both guidance branches and the update, float64 numpy: one whole "
+                      f"step of {fl / 1e12:.3f} TFLOP in {dt:.1f} s",
+            "ms_per_step": round(dt * 1e3, 1), **info}
 
 
 def run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q) -> int:
@@ -373,8 +397,33 @@ def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
 
     from paper_2509_04719_amd import _lib as L
     from paper_2509_04719_amd import schedule as psched
+    from seeded_inputs import configs
 
-    speeds = [float(v) for v in a.speeds.split(",")]
+    profile = None
+    if a.occupancy:
+        # Speeds from inference time profiles (§V-A): this GPU's band-step
+        # times over band heights; a virtual device with a co-tenant taking a
+        # share rho of it runs each step 1 / (1 - rho) times longer.
+        occ = [float(v) for v in a.occupancy.split(",")]
+        kv_p = torch.zeros(ctx.stale_kv_bytes() // 2, dtype=torch.bfloat16, device=x.device)
+        t, tp = configs.headline_timestep_pair(cfg)
+        base = []
+        for r in PROFILE_ROWS:
+            if r > cfg.R:
+                continue
+            o = torch.empty((cfg.in_ch, r * cfg.patch, cfg.latent), device=x.device)
+            m = _time_loop(torch, lambda: ctx.step(x, 0, r, t, tp, labels, cfg.cfg_scale, kv_p, 1, o),
+                           5, 2)
+            base.append((r, m))
+        del kv_p
+        profiles = [[(r, m / (1.0 - o)) for r, m in base] for o in occ]
+        ref = max(1, round(cfg.R / len(occ)))
+        speeds = L.speeds_from_profiles(profiles, ref)
+        profile = {"band_rows_ms": [[r, round(m, 4)] for r, m in base], "occupancy": occ,
+                   "ref_rows": ref, "speeds": [round(v, 4) for v in speeds]}
+        print(f"# profiled speeds: {json.dumps(profile)}", flush=True)
+    else:
+        speeds = [float(v) for v in a.speeds.split(",")]
     steps, rows = L.plan_devices(speeds, a.m_base, a.m_warmup, a.thr_a, a.thr_b, cfg.R)
     splits, tiers = [0], []
     for st, r in zip(steps, rows):
@@ -415,10 +464,11 @@ def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
     res = {"metric": "ms per image of the patch-parallel sampler on virtual devices", "value": round(ms, 2),
            "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": 1, "higher_is_better": False,
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-           "config": {"workload": f"{cfg.name}: {len(tiers)} virtual devices, speeds {speeds}, "
-                                  f"M_base {a.m_base}, M_warmup {a.m_warmup}, a {a.thr_a}, b {a.thr_b}",
+           "config": {"workload": f"{cfg.name}: {len(tiers)} virtual devices, speeds "
+                                  f"{[round(v, 4) for v in speeds]}, M_base {a.m_base}, M_warmup "
+                                  f"{a.m_warmup}, a {a.thr_a}, b {a.thr_b}",
                       "device_steps": steps, "device_rows": rows, "row_splits": splits,
-                      "tiers": tiers},
+                      "tiers": tiers, "speed_profile": profile},
            "tflops": round(flops / ms / 1e9, 1)}
     print(json.dumps(res), flush=True)
     ctx.close()
@@ -435,9 +485,11 @@ def main(argv=None) -> int:
     ap.add_argument("--kernel-iters", type=int, default=20)
     ap.add_argument("--op-split", action="store_true",
                     help="also time each hot kernel alone through the kernel-level entry points")
-    ap.add_argument("--cpu-blocks", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--sweep", action="store_true", help="also time the share sweep")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the share sweep (its other band shapes would mix into a "
+                         "profiler's per-kernel averages)")
+    ap.add_argument("--sweep-steps", type=int, default=10)
     ap.add_argument("--schedule", action="store_true",
                     help="time the whole sampler schedule of the band instead of one step "
                          "(the tiered schedule for configs that use it)")
@@ -445,6 +497,10 @@ def main(argv=None) -> int:
                     help="time the whole patch-parallel sampler over virtual devices planned "
                          "from --speeds (Algorithm 1 on this GPU)")
     ap.add_argument("--speeds", default="1.0,1.0,0.6,0.6")
+    ap.add_argument("--occupancy", default="",
+                    help="with --virtual-devices: derive the speeds from this GPU's measured "
+                         "band-step times, each virtual device slowed by a co-tenant taking "
+                         "the given share (comma list)")
     ap.add_argument("--m-base", type=int, default=50)
     ap.add_argument("--m-warmup", type=int, default=10)
     ap.add_argument("--thr-a", type=float, default=0.75)
@@ -486,9 +542,16 @@ def main(argv=None) -> int:
     x_np = generate.make_latent(cfg, 0)
     labels = generate.make_labels(cfg, 0)
     x = torch.from_numpy(x_np).to(dev)
-    stale = generate.make_stale_kv(cfg, 0)
-    kv = torch.from_numpy(stale.view(np.int16)).to(dev).view(torch.bfloat16)
     p = cfg.patch
+    # The stale buffer as Algorithm 1's synchronous warm-up leaves it: every
+    # token's K/V of a full-image step at the previous grid timestep, on an
+    # independent seeded latent.
+    kv = torch.zeros(ctx.stale_kv_bytes() // 2, dtype=torch.bfloat16, device=dev)
+    xs = torch.from_numpy(generate.make_stale_latent(cfg, 0)).to(dev)
+    full_out = torch.empty((cfg.in_ch, cfg.latent, cfg.latent), device=dev)
+    ctx.step(xs, 0, cfg.R, t + cfg.T // cfg.steps, t, labels, cfg.cfg_scale, kv, 1, full_out)
+    del xs, full_out
+    stale_np = generate.make_stale_kv(cfg, 0)      # oracle timing input (values do not matter)
     out = torch.empty((cfg.in_ch, rows * p, cfg.latent), device=dev)
 
     def one():
@@ -518,7 +581,7 @@ def main(argv=None) -> int:
     split = step_kernel_split(ctx, cfg, n_q, one, a.steps)
     dom = max(split, key=lambda k: split[k]["ms_per_step"])
     d = split[dom]
-    mfma_names = [k for k in ("qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm") if k in split]
+    mfma_names = [k for k in MFMA_KERNELS if k in split]
     mfma_flops = sum(split[k]["flop_per_launch"] * split[k]["launches_per_step"] for k in mfma_names)
     mfma_ms = sum(split[k]["ms_per_step"] for k in mfma_names)
     traffic = recorded_traffic(dom) if dom in KERNEL_SOURCES else None
@@ -537,18 +600,31 @@ def main(argv=None) -> int:
     print(f"# HBM-bound kernels at large shapes: {json.dumps(hbm)}", flush=True)
 
     sweep = {}
-    if a.sweep:
-        for share in (0.10, 0.25, 0.40, 0.65, 1.00):
+    if not a.no_sweep:
+        for share in SWEEP_SHARES:
             r = psched.band_rows(share, cfg.R)
             o = torch.empty((cfg.in_ch, r * p, cfg.latent), device=dev)
-            m = _time_loop(torch, lambda: ctx.step(x, 0, r, t, tp, labels, cfg.cfg_scale, kv, 1, o), 10, 2)
-            sweep[f"{int(share * 100)}%"] = {"rows": r, "ms": round(m, 3),
-                                            "tflops": round(step_flops(cfg, cfg.n_q(r)) / m / 1e9, 1)}
+
+            def band_step():
+                ctx.step(x, 0, r, t, tp, labels, cfg.cfg_scale, kv, 1, o)
+            m = _time_loop(torch, band_step, a.sweep_steps, 2)
+            ks = step_kernel_split(ctx, cfg, cfg.n_q(r), band_step, 3)
+            ag = [k for k in MFMA_KERNELS if k in ks]
+            ag_fl = sum(ks[k]["flop_per_launch"] * ks[k]["launches_per_step"] for k in ag)
+            ag_ms = sum(ks[k]["ms_per_step"] for k in ag)
+            sweep[f"{share:.0%}"] = {
+                "rows": r, "n_q": cfg.n_q(r), "ms": round(m, 3),
+                "tflops": round(step_flops(cfg, cfg.n_q(r)) / m / 1e9, 1),
+                "frac_of_bf16_peak": round(step_flops(cfg, cfg.n_q(r)) / m / 1e9 / PEAK_BF16_TFLOPS, 4),
+                "attn_gemm_tflops": round(ag_fl / ag_ms / 1e9, 1),
+                "attn_gemm_frac": round(ag_fl / ag_ms / 1e9 / PEAK_BF16_TFLOPS, 4),
+                "attention_tflops": ks["attention"]["tflops"]}
         print(f"# sweep: {json.dumps(sweep)}", flush=True)
 
     cpu = None
     if not a.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, blob, x_np, labels, stale, rb, re, t, tp, a.cpu_blocks)
+        r10 = psched.band_rows(CPU_SHARE, cfg.R)
+        cpu = cpu_baseline(cfg, blob, x_np, labels, stale_np, 0, r10, t, tp)
         print(f"# cpu baseline: {json.dumps(cpu)}", flush=True)
 
     res = {

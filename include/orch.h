@@ -183,6 +183,67 @@ int orch_schedule_coefficients(const orch_dit_config* cfg, int t, int t_prev, do
 int orch_plan_devices(const double* speed, int n, int m_base, int m_warmup, double a, double b,
                       int total_rows, int* steps_out, int* rows_out);
 
+/* ---- convolutional (U-Net) band block -------------------------------------
+ * The first half of a U-Net ResNet block, GroupNorm -> SiLU -> 3x3
+ * convolution (stride 1, zero padding 1, + bias), on a band of rows of one
+ * device's patch, with stale activation reuse (§II-B): a 3x3 convolution at
+ * the band's edge rows reads one row beyond each edge (halo rows, from the
+ * stale buffer of the convolution's input; zero outside the map), and the
+ * GroupNorm statistics of the whole map combine the band's fresh per-row
+ * partial sums with the stale partial sums of every other row.  GroupNorm has
+ * a per-channel affine (gamma, beta) and the biased variance
+ * (sum x^2)/N - mean^2 over the group's N elements of the whole map.
+ * Layouts are pixel-major (NHWC). */
+typedef struct {
+  int height, width;        /* feature map rows and columns                     */
+  int channels, groups;     /* C % 32 == 0, C % groups == 0, groups <= 256       */
+  int out_channels;         /* % 64 == 0                                         */
+  float eps;                /* GroupNorm epsilon, > 0                            */
+} orch_unet_conv_shape;
+
+/* Workspace bytes of orch_unet_conv_band for a band of band_rows rows. */
+size_t orch_unet_conv_workspace_bytes(const orch_unet_conv_shape* shape, int band_rows);
+
+/* GroupNorm -> SiLU -> conv3x3 on rows [row_begin, row_end) of the map.
+ *   x_band      device fp32 [r][W][C]: the block input on the band's rows.
+ *   gamma, beta device fp32 [C].
+ *   weight      device bf16 [C_out][3][3][C] (tap (dy, dx) reads input row
+ *               y + dy - 1, column x + dx - 1).
+ *   bias        device fp32 [C_out].
+ *   stale_act   device bf16 [H][W][C]: the convolution input of an earlier
+ *               step; rows row_begin - 1 and row_end are read (when inside
+ *               the map).  May be NULL for a band of every row without
+ *               refresh.
+ *   stale_sums  device fp32 [H][groups][2]: (sum, sum of squares) of x per
+ *               row and group of an earlier step; every row outside the band
+ *               is read.  May be NULL as stale_act.
+ *   refresh     != 0: the band's rows of stale_act receive this step's
+ *               activations (bf16) and of stale_sums its partial sums; other
+ *               rows are never written.
+ *   out         device fp32 [r][W][C_out].
+ *   workspace   device, >= orch_unet_conv_workspace_bytes(shape, r) bytes.
+ * Device pointers 16-byte aligned.  Errors: ORCH_EINVAL (shape, band, NULL
+ * pointer, alignment, workspace too small), ORCH_EHIP. */
+int orch_unet_conv_band(const orch_unet_conv_shape* shape, int row_begin, int row_end,
+                        const float* x_band, const float* gamma, const float* beta,
+                        const void* weight, const float* bias, void* stale_act,
+                        float* stale_sums, int refresh, float* out, void* workspace,
+                        size_t workspace_bytes, void* hip_stream);
+
+/* Host only: effective speeds for orch_plan_devices from inference time
+ * profiles (§V-A: speeds derived from historical inference times).  Device
+ * i has n_points[i] measured (band height, step time) pairs, taken in order
+ * from rows[] and ms[] (device 0's first).  Its times are fitted by least
+ * squares as t = alpha + beta * rows (a fixed per-step cost, the overhead
+ * that makes small patches inefficient, plus a per-row cost) and its speed is
+ * the rows per unit time at the reference band height:
+ * speed_out[i] = ref_rows / (alpha + beta * ref_rows).  With a single point,
+ * or one distinct height, alpha = 0.  Scaling a device's times by k divides
+ * its speed by k.  Errors: ORCH_EINVAL (no points, rows < 1, a time not
+ * finite and > 0, a non-positive fitted time at ref_rows). */
+int orch_speeds_from_profiles(int n, const int* n_points, const int* rows, const double* ms,
+                              int ref_rows, double* speed_out);
+
 /* Thread-local message describing the last error ("" if none). */
 const char* orch_last_error(void);
 

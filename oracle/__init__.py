@@ -18,10 +18,17 @@ Modules:
   dit      -- the DiT denoiser on an elastic band of token rows with stale
               K/V for the other rows (§II-B, Algorithm 1), classifier-free
               guidance, and the scheduler update.
+  allocator -- device planning: Eq. (2) tiers, Eq. (3) patch mending in
+              whole rows, effective speeds from step-time profiles (§V-A).
+  sampler  -- full-image and patch-parallel samplers (Algorithm 1 on virtual
+              devices).
+  unet     -- a U-Net block (GroupNorm -> SiLU -> conv3x3) on a band of rows
+              with stale halo rows and stale group statistics (§II-B).
 
 Parity status: the scheduler, attention, LayerNorm, GELU, sinusoid, patch
 embedding and unpatchify are pinned by the CPU tests; the DiT block as a
 whole is pinned against an independent torch-module DiT on the full image
 and by the invariants of the band step (all rows, stitching, locality,
-degenerate gates).
+degenerate gates); the U-Net block against torch's GroupNorm and conv2d and
+by the same invariants; the planner by the paper's tables.
 """

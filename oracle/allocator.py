@@ -29,9 +29,28 @@ from __future__ import annotations
 import math
 from typing import List, Sequence, Tuple
 
+import numpy as np
+
 
 def effective_speed(c: float, rho: float) -> float:
     return c * (1.0 - rho)
+
+
+def speed_from_profile(rows: Sequence[int], ms: Sequence[float], ref_rows: int) -> float:
+    """Effective speed from an inference time profile (§V-A: speeds derived
+    from historical inference times; the paper gives no formula).  Reading:
+    the step times are a fixed per-step cost plus a per-row cost, fitted by
+    least squares, t = alpha + beta * rows; the speed is the rows per unit time
+    at the reference band height, ref_rows / (alpha + beta * ref_rows).  A
+    single height fixes only beta = mean(t / rows) with alpha = 0."""
+    r = np.asarray(rows, dtype=np.float64)
+    t = np.asarray(ms, dtype=np.float64)
+    if np.all(r == r[0]):
+        alpha, beta = 0.0, t.sum() / r.sum()
+    else:
+        A = np.stack([np.ones_like(r), r], axis=1)
+        alpha, beta = np.linalg.lstsq(A, t, rcond=None)[0]
+    return ref_rows / (alpha + beta * ref_rows)
 
 
 def reduced_steps(M_base: int, M_warmup: int) -> int:

@@ -26,7 +26,8 @@ SYMBOLS = (
     "orch_attention_workspace_bytes", "orch_set_kernel_timing", "orch_kernel_times",
     "orch_linear_workspace_bytes",
     "orch_plan_devices", "orch_sample_patch_parallel", "orch_set_work_split",
-    "orch_op_attention_noalloc",
+    "orch_op_attention_noalloc", "orch_speeds_from_profiles", "orch_unet_conv_band",
+    "orch_unet_conv_workspace_bytes",
 )
 KCLASSES = ("conditioning", "patch_embed", "layernorm", "qkv_gemm", "attention", "proj_gemm",
             "fc1_gemm", "fc2_gemm", "final_layer", "update")
@@ -36,6 +37,11 @@ class OrchError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"orch error {code}: {msg}")
         self.code = code
+
+
+class UNetConvShape(C.Structure):
+    _fields_ = [("height", C.c_int), ("width", C.c_int), ("channels", C.c_int),
+                ("groups", C.c_int), ("out_channels", C.c_int), ("eps", C.c_float)]
 
 
 class OrchConfig(C.Structure):
@@ -83,6 +89,11 @@ def _load():
         "orch_op_patch_embed": (i, [vp, vp, i, i, vp, vp]),
         "orch_op_final_layer": (i, [vp, vp, i, i, vp, vp, vp]),
         "orch_plan_devices": (i, [C.POINTER(d), i, i, i, d, d, i, C.POINTER(i), C.POINTER(i)]),
+        "orch_speeds_from_profiles": (i, [i, C.POINTER(i), C.POINTER(i), C.POINTER(d), i,
+                                          C.POINTER(d)]),
+        "orch_unet_conv_workspace_bytes": (sz, [C.POINTER(UNetConvShape), i]),
+        "orch_unet_conv_band": (i, [C.POINTER(UNetConvShape), i, i, vp, vp, vp, vp, vp, vp, vp, i,
+                                    vp, vp, sz, vp]),
         "orch_sample_patch_parallel": (i, [vp, vp, i, C.POINTER(i), C.POINTER(i), C.POINTER(i), i, i,
                                            C.POINTER(i), f, vp, vp, vp]),
     }
@@ -132,6 +143,18 @@ def plan_devices(speeds, m_base, m_warmup, a, b, total_rows):
     rw = (C.c_int * n)()
     check(lib.orch_plan_devices(v, n, m_base, m_warmup, float(a), float(b), total_rows, st, rw))
     return list(st), list(rw)
+
+
+def speeds_from_profiles(profiles, ref_rows):
+    """Effective speeds from per-device [(rows, ms), ...] profiles (host only)."""
+    n = len(profiles)
+    pts = [pt for prof in profiles for pt in prof]
+    npts = (C.c_int * n)(*[len(prof) for prof in profiles])
+    rows = (C.c_int * len(pts))(*[int(r) for r, _ in pts])
+    ms = (C.c_double * len(pts))(*[float(t) for _, t in pts])
+    out = (C.c_double * n)()
+    check(lib.orch_speeds_from_profiles(n, npts, rows, ms, int(ref_rows), out))
+    return list(out)
 
 
 class DiTStep:
@@ -249,3 +272,20 @@ def attention(q, kv_stale, stale_bs, kv_fresh, fresh_bs, fresh_begin, n_fresh, B
     check(lib.orch_op_attention(_ptr(q), _ptr(kv_stale), stale_bs, _ptr(kv_fresh), fresh_bs,
                                 fresh_begin, n_fresh, B, heads, n_q, n_kv, head_dim, _ptr(out),
                                 _ptr(workspace), ws_bytes, dtype, _stream(stream)))
+
+
+def unet_shape(cfg, eps: float = 1e-5) -> UNetConvShape:
+    return UNetConvShape(cfg.height, cfg.width, cfg.channels, cfg.groups, cfg.out_channels, eps)
+
+
+def unet_conv_workspace_bytes(shape: UNetConvShape, band_rows: int) -> int:
+    return lib.orch_unet_conv_workspace_bytes(C.byref(shape), band_rows)
+
+
+def unet_conv_band(shape: UNetConvShape, row_begin, row_end, x_band, gamma, beta, weight, bias,
+                   stale_act, stale_sums, refresh, out, workspace, stream=None):
+    ws_bytes = workspace.numel() * workspace.element_size()
+    check(lib.orch_unet_conv_band(C.byref(shape), row_begin, row_end, _ptr(x_band), _ptr(gamma),
+                                  _ptr(beta), _ptr(weight), _ptr(bias), _ptr(stale_act),
+                                  _ptr(stale_sums), int(refresh), _ptr(out), _ptr(workspace),
+                                  ws_bytes, _stream(stream)))

@@ -19,8 +19,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liborch.so")
-SOURCES = ["k_gemm.hip", "k_attention.hip", "k_misc.hip", "orch_abi.hip", "orch_plan.hip",
-           "orch_noalloc.hip"]
+SOURCES = ["k_gemm.hip", "k_attention.hip", "k_misc.hip", "k_unet.hip", "orch_abi.hip",
+           "orch_plan.hip", "orch_noalloc.hip"]
 # per-source extra flags: attention is built without IEEE NaN quieting, so the
 # row max of the online softmax is plain v_max3_f32
 EXTRA = {"k_attention.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans"]}

@@ -130,4 +130,25 @@ hipError_t launch_update(const float* x, int ldx, const float* ec, const float* 
                          const float* z, int ldz, float a, float b, float c, float* out, int ldo,
                          int rows, size_t cols, hipStream_t stream);
 
+// U-Net band block: GroupNorm -> SiLU -> 3x3 convolution with stale halo
+// rows and stale group statistics (pixel-major layouts).
+struct UNetConvParams {
+  const float* x;             // fp32 [rows][W][C]: the band's block input
+  const float* gamma;         // fp32 [C]
+  const float* beta;          // fp32 [C]
+  const void* weight;         // bf16 [C_out][3][3][C]
+  const float* bias;          // fp32 [C_out]
+  void* stale_act;            // bf16 [H][W][C]: convolution input of an earlier step
+  float* stale_sums;          // fp32 [H][G][2]: per-row (sum, sum of squares)
+  float* out;                 // fp32 [rows][W][C_out]
+  int H, W, C, G, C_out, row_begin, row_end, refresh;
+  float eps;
+  // set by the launcher: workspace parts, and where the band's activations go
+  float* fresh_sums;          // fp32 [rows][G][2]
+  float* stats;               // fp32 [G][2]: mean, 1/sqrt(var + eps)
+  void* act_band;             // bf16 [rows][W][C]
+};
+size_t unet_conv_workspace_bytes(int W, int C, int G, int rows);
+hipError_t launch_unet_conv(const UNetConvParams& p, void* workspace, hipStream_t stream);
+
 }  // namespace orch

@@ -976,6 +976,62 @@ int orch_op_final_layer(orch_ctx* x, const float* h, int rb, int re, const float
   return run_final(x, h, rb, re, mod, out_eps, (hipStream_t)hip_stream);
 }
 
+namespace {
+int check_unet_shape(const orch_unet_conv_shape* s) {
+  if (!s) return fail(ORCH_EINVAL, "shape is NULL");
+  if (s->height < 1 || s->width < 1) return fail(ORCH_EINVAL, "height and width must be >= 1");
+  if (s->channels < 32 || s->channels % 32) return fail(ORCH_EINVAL, "channels must be a positive multiple of 32");
+  if (s->groups < 1 || s->groups > 256 || s->channels % s->groups)
+    return fail(ORCH_EINVAL, "groups must divide channels and be <= 256");
+  if (s->out_channels < 64 || s->out_channels % 64) return fail(ORCH_EINVAL, "out_channels must be a positive multiple of 64");
+  if (!(s->eps > 0.0f) || !std::isfinite(s->eps)) return fail(ORCH_EINVAL, "eps must be finite and > 0");
+  return ORCH_OK;
+}
+}  // namespace
+
+size_t orch_unet_conv_workspace_bytes(const orch_unet_conv_shape* s, int band_rows) {
+  if (!s || band_rows < 1 || s->groups < 1 || s->channels < 1) return 0;
+  return unet_conv_workspace_bytes(s->width, s->channels, s->groups, band_rows);
+}
+
+int orch_unet_conv_band(const orch_unet_conv_shape* s, int rb, int re, const float* x_band,
+                        const float* gamma, const float* beta, const void* weight,
+                        const float* bias, void* stale_act, float* stale_sums, int refresh,
+                        float* out, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  int rc = check_unet_shape(s);
+  if (rc) return rc;
+  if (rb < 0 || re <= rb || re > s->height)
+    return fail(ORCH_EINVAL, "band [%d, %d) not within [0, %d)", rb, re, s->height);
+  if (!x_band || !gamma || !beta || !weight || !bias || !out || !workspace)
+    return fail(ORCH_EINVAL, "NULL pointer");
+  const bool all_rows = rb == 0 && re == s->height;
+  if ((!all_rows || refresh) && (!stale_act || !stale_sums))
+    return fail(ORCH_EINVAL, "stale_act and stale_sums are needed unless the band is every row without refresh");
+  const int rows = re - rb;
+  const size_t need = unet_conv_workspace_bytes(s->width, s->channels, s->groups, rows);
+  if (workspace_bytes < need) return fail(ORCH_EINVAL, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  if (((uintptr_t)x_band | (uintptr_t)gamma | (uintptr_t)beta | (uintptr_t)weight | (uintptr_t)bias |
+       (uintptr_t)stale_act | (uintptr_t)stale_sums | (uintptr_t)out | (uintptr_t)workspace) & 15)
+    return fail(ORCH_EINVAL, "device buffers must be 16-byte aligned");
+  const size_t out_bytes = (size_t)rows * s->width * s->out_channels * 4;
+  const size_t x_bytes = (size_t)rows * s->width * s->channels * 4;
+  const size_t act_bytes = (size_t)s->height * s->width * s->channels * 2;
+  const size_t sums_bytes = (size_t)s->height * s->groups * 8;
+  if (ranges_overlap(out, out_bytes, x_band, x_bytes) || ranges_overlap(out, out_bytes, stale_act, act_bytes) ||
+      ranges_overlap(out, out_bytes, stale_sums, sums_bytes) || ranges_overlap(workspace, need, out, out_bytes) ||
+      ranges_overlap(workspace, need, stale_act, act_bytes) || ranges_overlap(workspace, need, x_band, x_bytes))
+    return fail(ORCH_EINVAL, "output or workspace overlaps an input");
+  hipError_t pending = hipGetLastError();
+  if (pending != hipSuccess) return hip_fail(pending, "earlier asynchronous error");
+  UNetConvParams p{};
+  p.x = x_band; p.gamma = gamma; p.beta = beta; p.weight = weight; p.bias = bias;
+  p.stale_act = stale_act; p.stale_sums = stale_sums; p.out = out;
+  p.H = s->height; p.W = s->width; p.C = s->channels; p.G = s->groups; p.C_out = s->out_channels;
+  p.row_begin = rb; p.row_end = re; p.refresh = refresh ? 1 : 0; p.eps = s->eps;
+  HIP_TRY(launch_unet_conv(p, workspace, (hipStream_t)hip_stream), "U-Net band launch");
+  return ORCH_OK;
+}
+
 int orch_set_work_split(orch_ctx* x, int enable) {
   if (!x) return fail(ORCH_EINVAL, "ctx is NULL");
   x->work_split = enable != 0;

@@ -64,3 +64,43 @@ int orch_plan_devices(const double* speed, int n, int m_base, int m_warmup, doub
   }
   return ORCH_OK;
 }
+
+// Effective speed of each device from its inference time profile: the
+// measured step times t_j at band heights r_j, fitted by least squares as
+// t = alpha + beta r (a fixed per-step cost plus a per-row cost), evaluated at
+// the reference band height: v = ref_rows / (alpha + beta ref_rows), rows per
+// unit of time.  One point (or one distinct height) gives beta = mean t / r.
+int orch_speeds_from_profiles(int n, const int* n_points, const int* rows, const double* ms,
+                              int ref_rows, double* speed_out) {
+  using orch_detail::set_error;
+  if (!n_points || !rows || !ms || !speed_out) return set_error(ORCH_EINVAL, "NULL argument");
+  if (n < 1 || ref_rows < 1) return set_error(ORCH_EINVAL, "need n >= 1 and ref_rows >= 1");
+  int off = 0;
+  std::vector<double> v(n);
+  for (int i = 0; i < n; ++i) {
+    const int k = n_points[i];
+    if (k < 1) return set_error(ORCH_EINVAL, "every device needs at least one profile point");
+    double sr = 0, st = 0, srr = 0, srt = 0;
+    bool distinct = false;
+    for (int j = off; j < off + k; ++j) {
+      if (rows[j] < 1 || !(ms[j] > 0.0) || !std::isfinite(ms[j]))
+        return set_error(ORCH_EINVAL, "profile points need rows >= 1 and finite times > 0");
+      distinct |= rows[j] != rows[off];
+      sr += rows[j]; st += ms[j]; srr += (double)rows[j] * rows[j]; srt += rows[j] * ms[j];
+    }
+    double alpha = 0.0, beta;
+    if (distinct) {
+      beta = (k * srt - sr * st) / (k * srr - sr * sr);
+      alpha = (st - beta * sr) / k;
+    } else {
+      beta = st / sr;
+    }
+    const double t_ref = alpha + beta * ref_rows;
+    if (!(t_ref > 0.0) || !std::isfinite(t_ref))
+      return set_error(ORCH_EINVAL, "fitted step time at the reference height is not positive");
+    v[i] = ref_rows / t_ref;
+    off += k;
+  }
+  for (int i = 0; i < n; ++i) speed_out[i] = v[i];
+  return ORCH_OK;
+}

@@ -137,3 +137,32 @@ def describe(cfg: DiTConfig, rows: Optional[int] = None) -> dict:
         d["band_rows"] = rows
         d["n_q"] = cfg.n_q(rows)
     return d
+
+
+# ---- convolutional (U-Net) band block --------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class UNetConvConfig:
+    """GroupNorm -> SiLU -> 3x3 convolution on an H x W feature map with C
+    channels (the first half of a U-Net ResNet block)."""
+    name: str
+    height: int
+    width: int
+    channels: int
+    groups: int
+    out_channels: int
+    band_rows: Tuple[int, ...] = ()
+    share_labels: Tuple[str, ...] = ()
+
+
+UNET_TINY = UNetConvConfig(name="unet_tiny", height=16, width=16, channels=64, groups=8,
+                           out_channels=64, band_rows=(5,), share_labels=("5/16 rows",))
+
+# The first stage of an SDXL-sized U-Net at 1024px: a 128 x 128 latent with
+# 320 channels in 32 groups.  The evaluation splits the latent into 32 patch
+# units (4 rows each); 18:14 units is its first two-GPU assignment.
+UNET_SDXL_1024 = UNetConvConfig(name="unet_sdxl_1024_stage1", height=128, width=128,
+                                channels=320, groups=32, out_channels=320,
+                                band_rows=(16, 56, 72), share_labels=("1/8", "14/32", "18/32"))
+
+UNET_CONFIGS = (UNET_TINY, UNET_SDXL_1024)

@@ -207,3 +207,30 @@ def make_stale_kv(cfg: DiTConfig, seed: int = 0, std: float | None = None) -> np
         v = (rng.standard_normal(e - s) * std).astype(np.float32)
         out[s:e] = v if cfg.dtype == "f32" else f32_to_bf16_bits(v)
     return out
+
+
+# ---- convolutional (U-Net) band block --------------------------------------
+# Seed streams of its own: parameters, input feature map.
+STREAM_UNET_PARAMS = 10
+STREAM_UNET_INPUT = 11
+
+
+def make_unet_params(cfg, seed: int = 0) -> dict:
+    """GroupNorm affine (gamma ~ 1 + N(0, 0.02^2), beta ~ N(0, 0.02^2)) fp32,
+    conv weight N(0, 0.02^2) as bf16 bits [C_out][3][3][C_in], bias fp32."""
+    rng = np.random.default_rng([seed, STREAM_UNET_PARAMS])
+    C, Co = cfg.channels, cfg.out_channels
+    gamma = (1.0 + rng.standard_normal(C) * INIT_STD).astype(np.float32)
+    beta = (rng.standard_normal(C) * INIT_STD).astype(np.float32)
+    w = (rng.standard_normal((Co, 3, 3, C)) * INIT_STD).astype(np.float32)
+    bias = (rng.standard_normal(Co) * INIT_STD).astype(np.float32)
+    return {"gamma": gamma, "beta": beta, "weight_bits": f32_to_bf16_bits(w), "bias": bias}
+
+
+def make_unet_input(cfg, seed: int = 0) -> np.ndarray:
+    """float32 [H][W][C] feature map: N(0, 1) plus a per-channel offset
+    N(0, 0.5^2), so the groups' means are not zero."""
+    rng = np.random.default_rng([seed, STREAM_UNET_INPUT])
+    off = rng.standard_normal(cfg.channels) * 0.5
+    x = rng.standard_normal((cfg.height, cfg.width, cfg.channels)) + off
+    return x.astype(np.float32)

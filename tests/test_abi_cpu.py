@@ -156,3 +156,29 @@ def test_linear_split_workspace(orch_lib, M, N, K, want):
     """Host-side k-split plan of the projection GEMM."""
     assert orch_lib.linear_workspace_bytes(M, N, K, 1) == want
     assert orch_lib.linear_workspace_bytes(M, N, K, 0) == 0   # fp32: no MFMA path
+
+
+def test_library_speeds_match_oracle(orch_lib):
+    rng = np.random.default_rng(3)
+    for trial in range(100):
+        n = int(rng.integers(1, 6))
+        profs = []
+        for _ in range(n):
+            k = int(rng.integers(1, 7))
+            rows = [int(r) for r in rng.integers(1, 129, k)]
+            a, b = rng.uniform(0.0, 3.0), rng.uniform(0.01, 0.5)
+            profs.append([(r, a + b * r + rng.uniform(-0.01, 0.01)) for r in rows])
+        ref = int(rng.integers(1, 129))
+        got = orch_lib.speeds_from_profiles(profs, ref)
+        want = [oal.speed_from_profile([r for r, _ in p], [t for _, t in p], ref) for p in profs]
+        np.testing.assert_allclose(got, want, rtol=1e-9)
+
+
+@pytest.mark.parametrize("profs,ref,word", [
+    ([[]], 8, "at least one"), ([[(0, 1.0)]], 8, "rows >= 1"), ([[(4, -1.0)]], 8, "times > 0"),
+    ([[(4, 1.0)]], 0, "ref_rows"), ([[(4, 10.0), (8, 1.0)]], 64, "not positive"),
+])
+def test_library_speeds_reject(orch_lib, profs, ref, word):
+    with pytest.raises(orch_lib.OrchError) as e:
+        orch_lib.speeds_from_profiles(profs, ref)
+    assert e.value.code == orch_lib.ORCH_EINVAL and word in orch_lib.last_error()

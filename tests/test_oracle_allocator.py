@@ -86,3 +86,37 @@ def test_whole_rows_largest_remainder():
         s = rng.dirichlet(np.ones(5))
         r = al.whole_rows(list(s), 61)
         assert sum(r) == 61 and all(abs(ri - si * 61) < 1 for ri, si in zip(r, s))
+
+
+def test_speed_from_profile_pins():
+    """Synthetic profiles whose speeds follow from the definition by hand."""
+    # exactly linear: t = 2 + 0.5 r  -> at r = 16: 16 / 10
+    rows = [4, 8, 16, 32]
+    t = [2 + 0.5 * r for r in rows]
+    assert abs(al.speed_from_profile(rows, t, 16) - 1.6) < 1e-12
+    # no fixed cost: the speed is 1 / beta at any reference height
+    assert abs(al.speed_from_profile(rows, [0.25 * r for r in rows], 7) - 4.0) < 1e-12
+    # a device k times slower (an occupancy of 1 - 1/k) has 1/k of the speed
+    s1 = al.speed_from_profile(rows, t, 16)
+    s3 = al.speed_from_profile(rows, [3 * x for x in t], 16)
+    assert abs(s1 / s3 - 3.0) < 1e-12
+    # the fixed cost makes the speed depend on the reference height
+    assert al.speed_from_profile(rows, t, 4) < al.speed_from_profile(rows, t, 32)
+    # a single height: alpha = 0
+    assert abs(al.speed_from_profile([10, 10], [4.0, 6.0], 3) - 2.0) < 1e-12
+    # noise around a line: the least-squares fit recovers it exactly for
+    # symmetric residuals
+    tn = [x + e for x, e in zip(t, [0.1, -0.1, -0.1, 0.1])]
+    r = np.array(rows, float)
+    fit = np.polyfit(r, tn, 1)
+    assert abs(al.speed_from_profile(rows, tn, 16) - 16 / np.polyval(fit, 16)) < 1e-12
+
+
+def test_profiled_speeds_reproduce_occupancy_speeds():
+    """Profiles of one device scaled by 1/(1 - rho) give speeds proportional
+    to 1 - rho, so the plan equals the occupancy plan."""
+    rows = [4, 8, 16, 32, 64]
+    t = [0.8 + 0.2 * r for r in rows]
+    occ = [0.0, 0.4]
+    v = [al.speed_from_profile(rows, [x / (1 - o) for x in t], 16) for o in occ]
+    assert al.plan(v, 100, 4, 0.75, 0.25, 32) == al.plan([1 - o for o in occ], 100, 4, 0.75, 0.25, 32)

@@ -138,3 +138,78 @@ def test_mutation_guidance_branch_swap(model, monkeypatch):
         return eps[0] + cfg_scale * (eps[1] - eps[0])
     monkeypatch.setattr(dit, "guided_eps", swapped)
     assert not _branch_order_holds(hdr, params, x, labels)
+
+
+# ---- U-Net band block -------------------------------------------------------
+
+def _unet_pins_hold():
+    """The torch pin (full map) and the stitching pin (bands with the full
+    map's own buffers) of the U-Net band block."""
+    from oracle import unet
+    from oracle.blob import bf16_to_float
+    from tests.test_oracle_unet import _torch_block
+    cfg = configs.UNET_TINY
+    pr = generate.make_unet_params(cfg, 0)
+    params = {"gamma": pr["gamma"].astype(np.float64), "beta": pr["beta"].astype(np.float64),
+              "weight": bf16_to_float(pr["weight_bits"]).astype(np.float64),
+              "bias": pr["bias"].astype(np.float64)}
+    x = generate.make_unet_input(cfg, 0).astype(np.float64)
+    full = unet.full_step(params, x, cfg.groups)
+    ok = np.allclose(full["out"], _torch_block(params, x, cfg.groups)[0], rtol=1e-10, atol=1e-10)
+    sums = unet.row_group_sums(x, cfg.groups)
+    for rb, re in ((0, 5), (5, 11), (11, 16)):
+        got = unet.band_step(params, x[rb:re], cfg.height, rb, re, cfg.groups, full["act"], sums)
+        ok &= bool(np.allclose(got["out"], full["out"][rb:re], rtol=1e-10, atol=1e-10))
+    return bool(ok)
+
+
+def test_unet_mutation_halo_off_by_one(monkeypatch):
+    from oracle import unet
+    assert _unet_pins_hold()
+    orig = unet.band_step
+
+    def wrong(params, x_band, H, rb, re, groups, stale_act=None, stale_sums=None, eps=unet.GN_EPS):
+        if stale_act is not None:                 # halo taken one row too far out
+            stale_act = np.concatenate([stale_act[1:], stale_act[-1:]])
+        return orig(params, x_band, H, rb, re, groups, stale_act, stale_sums, eps)
+    monkeypatch.setattr(unet, "band_step", wrong)
+    assert not _unet_pins_hold()
+
+
+@pytest.mark.parametrize("slip", ["band_only_stats", "unbiased_var", "wrapped_columns",
+                                  "no_silu"])
+def test_unet_mutations(monkeypatch, slip):
+    from oracle import unet
+    assert _unet_pins_hold()
+    if slip == "band_only_stats":
+        orig = unet.group_stats
+
+        def wrong(sums, W, C, eps=unet.GN_EPS):
+            s = np.asarray(sums)
+            keep = ~np.isclose(s, 0).all(axis=(1, 2))
+            return orig(s[keep][:max(1, len(s) // 3)], W, C, eps)
+        monkeypatch.setattr(unet, "group_stats", wrong)
+    elif slip == "unbiased_var":
+        orig = unet.group_stats
+
+        def wrong(sums, W, C, eps=unet.GN_EPS):
+            s = np.asarray(sums, dtype=np.float64)
+            n = s.shape[0] * W * (C // s.shape[1])
+            mean, rstd = orig(sums, W, C, eps)
+            var = (1 / rstd ** 2 - eps) * n / (n - 1)
+            return mean, 1 / np.sqrt(var + eps)
+        monkeypatch.setattr(unet, "group_stats", wrong)
+    elif slip == "wrapped_columns":
+        def wrong(act_rows, weight, bias):
+            a = np.asarray(act_rows, dtype=np.float64)
+            r = a.shape[0] - 2
+            out = np.zeros((r, a.shape[1], weight.shape[0])) + bias
+            for dy in range(3):
+                for dx in range(3):
+                    win = np.roll(a[dy:dy + r], 1 - dx, axis=1)
+                    out += win @ weight[:, dy, dx, :].T
+            return out
+        monkeypatch.setattr(unet, "conv3x3_rows", wrong)
+    else:
+        monkeypatch.setattr(unet, "silu", lambda v: v)           # GroupNorm output as is
+    assert not _unet_pins_hold()
