@@ -475,6 +475,45 @@ def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
     return 0
 
 
+def run_unet(a) -> int:
+    """The U-Net band block (GroupNorm -> SiLU -> conv3x3 with stale halo rows
+    and stale group statistics) on SDXL's first stage at 1024px: ms per call
+    and the convolution's TFLOP/s per band."""
+    import numpy as np
+    import torch
+
+    from paper_2509_04719_amd import _lib as L
+    from seeded_inputs import configs, generate
+
+    cfg = configs.UNET_SDXL_1024
+    dev = "cuda:0"
+    H, W, C, Co, G = cfg.height, cfg.width, cfg.channels, cfg.out_channels, cfg.groups
+    shape = L.unet_shape(cfg)
+    pr = generate.make_unet_params(cfg, 0)
+    x = torch.from_numpy(generate.make_unet_input(cfg, 0)).to(dev)
+    gamma, beta, bias = (torch.from_numpy(pr[k]).to(dev) for k in ("gamma", "beta", "bias"))
+    wt = torch.from_numpy(pr["weight_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+    act = torch.zeros((H, W, C), dtype=torch.bfloat16, device=dev)
+    sums = torch.zeros((H, G, 2), device=dev)
+    ws = torch.empty(L.unet_conv_workspace_bytes(shape, H), dtype=torch.uint8, device=dev)
+    full = torch.empty((H, W, Co), device=dev)
+    L.unet_conv_band(shape, 0, H, x, gamma, beta, wt, bias, act, sums, 1, full, ws)   # fill buffers
+    res = {}
+    for rb, re in [(56, 72), (0, 56), (56, 128), (0, H)]:
+        r = re - rb
+        xb = x[rb:re].contiguous()
+        o = torch.empty((r, W, Co), device=dev)
+        ms = _time_loop(torch, lambda: L.unet_conv_band(shape, rb, re, xb, gamma, beta, wt, bias, act,
+                                                        sums, 1, o, ws), a.steps)
+        fl = 2.0 * r * W * Co * 9 * C
+        res[f"[{rb},{re})"] = {"rows": r, "ms": round(ms, 4), "conv_tflops": round(fl / ms / 1e9, 1)}
+    out = {"metric": "U-Net band block ms (GroupNorm, SiLU, conv3x3), SDXL stage 1 at 1024px",
+           "unit": "ms", "config": {"workload": f"{cfg.name}: {H}x{W}x{C}, {G} groups -> {Co}"},
+           "bands": res}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -505,6 +544,8 @@ def main(argv=None) -> int:
     ap.add_argument("--m-warmup", type=int, default=10)
     ap.add_argument("--thr-a", type=float, default=0.75)
     ap.add_argument("--thr-b", type=float, default=0.25)
+    ap.add_argument("--unet", action="store_true",
+                    help="time the U-Net band block (SDXL first stage at 1024px) instead")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run the workload of the HBM counter runs and exit")
     ap.add_argument("--pmc-report", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -529,6 +570,8 @@ def main(argv=None) -> int:
         return 1
     if a.pmc_probe:
         return pmc_probe(a)
+    if a.unet:
+        return run_unet(a)
     dev = "cuda:0"
     cfg = configs.get(a.config)
     rows = psched.band_rows(a.share, cfg.R)
