@@ -22,7 +22,7 @@ leaves these open for a simulation on one machine):
 """
 from __future__ import annotations
 
-from typing import Sequence
+from typing import Optional, Sequence
 
 import numpy as np
 
@@ -40,8 +40,12 @@ def full_sample(hdr, params, x_T, t_grid: Sequence[int], labels, cfg_scale: floa
 
 def patch_parallel_sample(hdr, params, x_T, splits: Sequence[int], tiers: Sequence[int],
                           t_grid: Sequence[int], warmup: int, labels, cfg_scale: float,
-                          dtype=np.float64):
-    """Algorithm 1 on len(tiers) virtual devices; returns the final latent."""
+                          dtype=np.float64, order: Optional[Sequence[int]] = None):
+    """Algorithm 1 on len(tiers) virtual devices; returns the final latent.
+
+    order: the order in which this simulation visits the devices within an
+    interval (default: by index).  The devices of Algorithm 1 run in
+    parallel, so the result does not depend on it."""
     M = len(t_grid) - 1
     if not 1 <= warmup <= M:
         raise ValueError("need 1 <= warmup <= steps")
@@ -58,7 +62,8 @@ def patch_parallel_sample(hdr, params, x_T, splits: Sequence[int], tiers: Sequen
         m2 = min(m + 2, M)
         nxt = buf.copy()
         x_next = x.copy()
-        for i, tier in enumerate(tiers):
+        for i in (range(len(tiers)) if order is None else order):
+            tier = tiers[i]
             rb, re = splits[i], splits[i + 1]
             rows = slice(rb * p, re * p)
             if tier == 0 and m2 == m + 2:

@@ -213,3 +213,61 @@ def test_unet_mutations(monkeypatch, slip):
     else:
         monkeypatch.setattr(unet, "silu", lambda v: v)           # GroupNorm output as is
     assert not _unet_pins_hold()
+
+
+# ---- patch-parallel sampler (Algorithm 1 on virtual devices) -----------------
+
+def _sampler_pins_hold():
+    from oracle import sampler
+    from oracle import schedule as osched
+    cfg = configs.TINY
+    hdr, params = oblob.read_blob(generate.make_weight_blob(cfg, 0))
+    x, lab = generate.make_latent(cfg, 1), generate.make_labels(cfg, 1)
+    g = [t for t, _ in osched.step_pairs(cfg.T, 7)] + [-1]
+    splits = [0, 3, 5, cfg.R]
+    ok = True
+    for tiers in ([0, 0, 1], [1, 0, 0]):
+        a = sampler.patch_parallel_sample(hdr, params, x, splits, tiers, g, 2, lab, 1.5)
+        b = sampler.patch_parallel_sample(hdr, params, x, splits, tiers, g, 2, lab, 1.5, order=[2, 0, 1])
+        ok &= bool(np.array_equal(a, b))
+    g6 = [t for t, _ in osched.step_pairs(cfg.T, 6)] + [-1]
+    one = sampler.patch_parallel_sample(hdr, params, x, [0, cfg.R], [0], g6, 2, lab, 1.5)
+    ok &= bool(np.array_equal(one, sampler.full_sample(hdr, params, x, g6, lab, 1.5)))
+    return ok
+
+
+@pytest.mark.parametrize("slip", ["second_half_reads_exchanged", "second_half_from_interval_start",
+                                  "reduced_tier_reads_exchanged"])
+def test_sampler_mutations(monkeypatch, slip):
+    """Plausible slips in which buffer or latent a half-step reads break the
+    device-order invariance or the one-device reduction to the full sampler.
+    In the sampler, a band step that keeps its K/V is one whose K/V are
+    exchanged (a tier-0 first half-step or a tier-1 double step); the tier-0
+    second half-step keeps nothing."""
+    from oracle import sampler  # noqa: F401  (the pins run it)
+    assert _sampler_pins_hold()
+    orig_step, orig_refreshed = dit.patch_step, dit.refreshed_buffer
+    interval = 1000 // 7                            # grid spacing of the pins' 7-step grid
+    state = {}
+
+    def refreshed(hdr, stale, kv, rb, re, dtype=np.float64):
+        state["exchanged"] = orig_refreshed(hdr, stale, kv, rb, re, dtype)   # the next buffer so far
+        return state["exchanged"]
+
+    def step(hdr, params, x_full, rb, re, t, tp, labels, g, stale_kv=None, **kw):
+        exchanges = kw.get("keep_kv", False)
+        double = tp == -1 or t - tp > 1.5 * interval
+        if stale_kv is not None and "exchanged" in state:
+            if slip == "second_half_reads_exchanged" and not exchanges:
+                stale_kv = state["exchanged"]
+            if slip == "reduced_tier_reads_exchanged" and exchanges and double:
+                stale_kv = state["exchanged"]
+        if slip == "second_half_from_interval_start" and not exchanges and stale_kv is not None:
+            x_full = state.get("x_first_half", x_full)
+        if exchanges:
+            state["x_first_half"] = x_full
+        return orig_step(hdr, params, x_full, rb, re, t, tp, labels, g, stale_kv, **kw)
+
+    monkeypatch.setattr(dit, "refreshed_buffer", refreshed)
+    monkeypatch.setattr(dit, "patch_step", step)
+    assert not _sampler_pins_hold()

@@ -71,3 +71,17 @@ def test_error_to_full_sampler_is_order_one_over_M(model, tiers):
     assert errs[0] > 0
     for e1, e2 in zip(errs, errs[1:]):
         assert 0.35 < e2 / e1 < 0.65, errs
+
+
+@pytest.mark.parametrize("tiers", [[0, 0, 1], [1, 0, 0]])
+def test_device_order_does_not_matter(model, tiers):
+    """Algorithm 1's devices run in parallel: visiting them in another order
+    within an interval gives the same latent bit for bit."""
+    hdr, params = model
+    x, lab = _inputs()
+    g = _grid(7)
+    splits = [0, 3, 5, CFG.R]
+    a = sampler.patch_parallel_sample(hdr, params, x, splits, tiers, g, 2, lab, CFG.cfg_scale)
+    b = sampler.patch_parallel_sample(hdr, params, x, splits, tiers, g, 2, lab, CFG.cfg_scale,
+                                      order=[2, 0, 1])
+    assert np.array_equal(a, b)
