@@ -196,7 +196,7 @@ int orch_plan_devices(const double* speed, int n, int m_base, int m_warmup, doub
  * Layouts are pixel-major (NHWC). */
 typedef struct {
   int height, width;        /* feature map rows and columns                     */
-  int channels, groups;     /* C % 32 == 0, C % groups == 0, groups <= 256       */
+  int channels, groups;     /* C % 64 == 0, C % groups == 0, groups <= 256       */
   int out_channels;         /* % 64 == 0                                         */
   float eps;                /* GroupNorm epsilon, > 0                            */
 } orch_unet_conv_shape;

@@ -46,7 +46,7 @@ __device__ __forceinline__ float gelu_tanh_f(float x) {
   return 0.5f * x * (1.0f + tanhf(k0 * (x + k1 * x * x * x)));
 }
 
-inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+__host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // max of v over lanes l and l ^ 32, on the VALU (v_permlane32_swap: lane l
 // of the first result holds v[l & 31], of the second v[l | 32])

@@ -25,20 +25,26 @@ namespace orch {
 
 // ---------------------------------------------------------------------------
 // 1. Partial sums of one band row.  A thread owns one channel quad and walks
-// a share of the row's pixels; the shares meet in LDS and are added in a
-// fixed order (the sums are bitwise reproducible), then per group.
-__global__ __launch_bounds__(256) void gn_row_sums_kernel(UNetConvParams p) {
-  extern __shared__ float s_part[];          // [per][C][2]
+// a share of the row's pixels (1024 threads: about a dozen shares, so each
+// thread has a few independent loads in flight); the shares meet in LDS and
+// are added in a fixed order (the sums are bitwise reproducible), then per
+// group.
+constexpr int kRowSumThreads = 1024;
+
+__global__ __launch_bounds__(kRowSumThreads) void gn_row_sums_kernel(UNetConvParams p) {
+  extern __shared__ float s_part[];          // [shares][C][2]
   const int y = blockIdx.x;
   const int C = p.C, W = p.W, Q = C / 4;
-  // Q <= 256: 256 / Q pixel shares, one quad per thread; wider rows: one
-  // share, a thread takes quads tid, tid + 256, ...
-  const int per = Q <= 256 ? 256 / Q : 1;
-  const int p0 = Q <= 256 ? threadIdx.x / Q : 0;
+  // Q <= threads: threads / Q pixel shares, one quad per thread; wider rows:
+  // one share, a thread takes quads tid, tid + threads, ...
+  const int per = Q <= kRowSumThreads ? kRowSumThreads / Q : 1;
+  const int p0 = Q <= kRowSumThreads ? threadIdx.x / Q : 0;
   const float4* row = reinterpret_cast<const float4*>(p.x + (size_t)y * W * C);
   if (p0 < per) {
-    for (int q = Q <= 256 ? threadIdx.x % Q : threadIdx.x; q < Q; q += Q <= 256 ? Q : 256) {
+    for (int q = Q <= kRowSumThreads ? threadIdx.x % Q : threadIdx.x; q < Q;
+         q += Q <= kRowSumThreads ? Q : kRowSumThreads) {
       float s[4] = {0, 0, 0, 0}, ss[4] = {0, 0, 0, 0};
+#pragma unroll 4
       for (int x = p0; x < W; x += per) {
         const float4 v = row[(size_t)x * Q + q];
         s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
@@ -54,7 +60,7 @@ __global__ __launch_bounds__(256) void gn_row_sums_kernel(UNetConvParams p) {
   }
   __syncthreads();
   const int cg = C / p.G;
-  for (int g = threadIdx.x; g < p.G; g += 256) {
+  for (int g = threadIdx.x; g < p.G; g += kRowSumThreads) {
     float a = 0.0f, b = 0.0f;
     for (int c = g * cg; c < (g + 1) * cg; ++c)
       for (int k = 0; k < per; ++k) {
@@ -68,23 +74,42 @@ __global__ __launch_bounds__(256) void gn_row_sums_kernel(UNetConvParams p) {
 }
 
 // 2. Group statistics over the whole map: band rows from the fresh sums,
-// every other row from the stale sums.
+// every other row from the stale sums.  256 / G threads per group each add
+// a stride of the rows (independent loads), then the group's shares are
+// added in a fixed order, in float64.
 __global__ __launch_bounds__(256) void gn_stats_kernel(UNetConvParams p) {
-  const int g = threadIdx.x;
-  if (g >= p.G) return;
-  double s = 0.0, q = 0.0;
+  __shared__ double red[256][2];
+  const int t = threadIdx.x;
+  // the convolution's zero page (read for taps outside the map)
+  if (t < 64) reinterpret_cast<float*>(p.zero_page)[t] = 0.0f;
+  const int per = 256 / p.G;                  // G <= 256
+  const int g = t % p.G, part = t / p.G;
   const float2* st = reinterpret_cast<const float2*>(p.stale_sums);
   const float2* fr = reinterpret_cast<const float2*>(p.fresh_sums);
-  for (int y = 0; y < p.H; ++y) {
-    const bool band = y >= p.row_begin && y < p.row_end;
-    const float2 v = band ? fr[(size_t)(y - p.row_begin) * p.G + g] : st[(size_t)y * p.G + g];
-    s += v.x;
-    q += v.y;
+  double s = 0.0, q = 0.0;
+  if (part < per) {
+#pragma unroll 4
+    for (int y = part; y < p.H; y += per) {
+      const bool band = y >= p.row_begin && y < p.row_end;
+      const float2 v = band ? fr[(size_t)(y - p.row_begin) * p.G + g] : st[(size_t)y * p.G + g];
+      s += v.x;
+      q += v.y;
+    }
+  }
+  red[t][0] = s;
+  red[t][1] = q;
+  __syncthreads();
+  if (t >= p.G) return;
+  s = 0.0;
+  q = 0.0;
+  for (int k = 0; k < per; ++k) {
+    s += red[k * p.G + t][0];
+    q += red[k * p.G + t][1];
   }
   const double n = (double)p.H * p.W * (p.C / p.G);
   const double mean = s / n;
   const double var = q / n - mean * mean;
-  reinterpret_cast<float2*>(p.stats)[g] =
+  reinterpret_cast<float2*>(p.stats)[t] =
       make_float2((float)mean, (float)(1.0 / sqrt(var + (double)p.eps)));
 }
 
@@ -111,67 +136,102 @@ __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// 4. The convolution.  Workgroup tile: 128 band pixels x 64 output channels,
-// four waves of 32 pixels each; k-tiles of one tap x 32 input channels, staged
-// through registers into double-buffered LDS (rows of 32 channels padded to
-// 40, so the 16-byte fragment reads of 16 rows land on distinct banks).  The
-// MFMAs take the weight rows as the first operand, so a lane ends with four
-// consecutive output channels of one pixel: one 16-byte store each.
+// 4. The convolution as an implicit GEMM.  Workgroup tile: 128 band pixels x
+// 64 output channels, four waves of 32 pixels; k-tiles of one tap x 64 input
+// channels (128-byte rows), loaded straight into LDS (16 bytes per lane, no
+// register staging) into a ring of three stages, one barrier per k-tile.  A
+// lane of a wave-level load fills LDS row (lane / 8) of its 8-row slab at
+// physical chunk lane % 8, holding logical chunk (lane % 8) ^ ((row / 2) % 8):
+// the fragment reads (16 rows at one logical chunk) then hit distinct banks.
+// The A rows are gathered per tap: the pixel shifted by (dy - 1, dx - 1),
+// read from the band's activations, the stale buffer (halo rows) or a zero
+// page (outside the map).  The MFMAs take the weight rows as the first
+// operand, so a lane ends with four consecutive output channels of one pixel.
+// Short bands split the nine taps in three groups of three (one per kernel
+// row dy) over more workgroups; their fp32 partial sums are added in order by
+// a second kernel, which adds the bias.
 namespace conv {
-constexpr int BM = 128, BN = 64, BK = 32, LDR = BK + 8;
+constexpr int BM = 128, BN = 64, BK = 64, S = 3, NW = 4;
+constexpr int ROWB = 2 * BK;                         // bytes per LDS row
+constexpr int STAGE = (BM + BN) * ROWB;              // 24 KB
+constexpr int LA = BM * ROWB / (NW * 1024);          // A loads per lane per k-tile (4)
+constexpr int LB = BN * ROWB / (NW * 1024);          // B loads per lane per k-tile (2)
+constexpr int LPT = LA + LB;
+constexpr int SPLITS = 3;                            // tap groups of a split launch
 }
 
-__global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p) {
+template <int LPTn>
+__device__ __forceinline__ void conv_wait(int tiles_after) {
+  if (tiles_after >= 2) wait_vmcnt<2 * LPTn>();
+  else if (tiles_after == 1) wait_vmcnt<LPTn>();
+  else wait_vmcnt<0>();
+}
+
+__global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p, int splits) {
   using namespace conv;
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM][LDR];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN][LDR];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rows = p.row_end - p.row_begin;
   const int M = rows * p.W;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int tiles_n = p.C_out / BN;
+  const int tiles = ceil_div(M, BM) * tiles_n;
+  const int split = __builtin_amdgcn_readfirstlane((int)blockIdx.x / tiles);
+  const int tile = blockIdx.x - split * tiles;
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
   const int C = p.C, W = p.W;
-  const int kc = C / BK, KT = 9 * kc;
-  const bf16* act_band = reinterpret_cast<const bf16*>(p.act_band);
-  const bf16* stale = reinterpret_cast<const bf16*>(p.stale_act);
-  const bf16* wgt = reinterpret_cast<const bf16*>(p.weight);
+  const int kc = C / BK;                               // channel chunks per tap
+  const int tap0 = split * 9 / splits, ntap = (split + 1) * 9 / splits - tap0;
+  const int KT = ntap * kc;
+  const char* act_band = reinterpret_cast<const char*>(p.act_band);
+  const char* stale = reinterpret_cast<const char*>(p.stale_act);
+  const char* zero = reinterpret_cast<const char*>(p.zero_page);
+  const char* wgt = reinterpret_cast<const char*>(p.weight);
 
-  // loader roles: A chunks j = tid + 256 e (row j / 4, 16-byte chunk j % 4),
-  // B chunk tid (row tid / 4, chunk tid % 4)
-  int ay[2], ax[2];
-  bool aon[2];
+  // this lane's load slots: A rows 8 (i NW + wave) + lane / 8 (pixel of the
+  // tile), B rows likewise (output channel); logical chunk of the slot
+  const int lrow = lane >> 3, pc = lane & 7;
+  int ay[LA], ax[LA], alc[LA];
+  bool aon[LA];
 #pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int m = m0 + ((tid + 256 * e) >> 2);
-    aon[e] = m < M;
-    const int mm = aon[e] ? m : 0;
-    ay[e] = p.row_begin + mm / W;
-    ax[e] = mm % W;
+  for (int i = 0; i < LA; ++i) {
+    const int r = 8 * (i * NW + wave) + lrow;
+    const int m = m0 + r;
+    aon[i] = m < M;
+    const int mm = aon[i] ? m : 0;
+    ay[i] = p.row_begin + mm / W;
+    ax[i] = mm % W;
+    alc[i] = pc ^ ((r >> 1) & 7);
   }
-  const int ach = (tid & 3) * 8;               // channel offset of this thread's chunks
-  const int brow = tid >> 2;
-  uint4 ra[2], rw;
+  size_t boff[LB];
+#pragma unroll
+  for (int i = 0; i < LB; ++i) {
+    const int r = 8 * (i * NW + wave) + lrow;
+    boff[i] = ((size_t)(n0 + r) * 9 * C + (size_t)(pc ^ ((r >> 1) & 7)) * 8) * 2;
+  }
 
-  auto load = [&](int kt) {
-    const int tap = kt / kc, c0 = (kt - tap * kc) * BK;
+  auto issue = [&](int kt, int st) {
+    const int tap = tap0 + kt / kc, c0 = (kt % kc) * BK;
     const int dy = tap / 3 - 1, dx = tap % 3 - 1;
+    char* base = smem + st * STAGE;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int sy = ay[e] + dy, sx = ax[e] + dx;
-      ra[e] = make_uint4(0, 0, 0, 0);
-      if (aon[e] && sx >= 0 && sx < W && sy >= 0 && sy < p.H) {
-        const bf16* src = (sy >= p.row_begin && sy < p.row_end)
-                              ? act_band + ((size_t)(sy - p.row_begin) * W + sx) * C
-                              : stale + ((size_t)sy * W + sx) * C;
-        ra[e] = *reinterpret_cast<const uint4*>(src + c0 + ach);
+    for (int i = 0; i < LA; ++i) {
+      const int sy = ay[i] + dy, sx = ax[i] + dx;
+      const char* src = zero;
+      if (aon[i] && sx >= 0 && sx < W && sy >= 0 && sy < p.H) {
+        src = (sy >= p.row_begin && sy < p.row_end)
+                  ? act_band + (((size_t)(sy - p.row_begin) * W + sx) * C + c0 + alc[i] * 8) * 2
+                  : stale + (((size_t)sy * W + sx) * C + c0 + alc[i] * 8) * 2;
       }
+      __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src,
+                                       (ORCH_LDS void*)(base + (i * NW + wave) * 1024), 16, 0, 0);
     }
-    rw = *reinterpret_cast<const uint4*>(wgt + ((size_t)(n0 + brow) * 9 + tap) * C + c0 + ach);
-  };
-  auto store = [&](int buf) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e)
-      *reinterpret_cast<uint4*>(&sA[buf][(tid + 256 * e) >> 2][ach]) = ra[e];
-    *reinterpret_cast<uint4*>(&sB[buf][brow][ach]) = rw;
+    for (int i = 0; i < LB; ++i) {
+      const char* src = wgt + boff[i] + ((size_t)tap * C + c0) * 2;
+      __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src,
+                                       (ORCH_LDS void*)(base + BM * ROWB + (i * NW + wave) * 1024), 16, 0, 0);
+    }
   };
 
   f32x16 acc[2];
@@ -180,37 +240,44 @@ __global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
 
-  load(0);
-  store(0);
-  __syncthreads();
-  const int frow = lane & 31, fk = 8 * (lane >> 5);
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) load(kt + 1);
+  // fragment reads: A row 32 wave + (lane & 31), B rows 32 j + (lane & 31),
+  // logical chunk 2 kk + (lane >> 5)
+  const int frow = lane & 31, h = lane >> 5;
+  const int arow = (32 * wave + frow) * ROWB, brow = BM * ROWB + frow * ROWB;
+  int koff[BK / 16];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const bf16x8 fa = *reinterpret_cast<const bf16x8*>(&sA[cur][32 * wave + frow][16 * ks + fk]);
+  for (int kk = 0; kk < BK / 16; ++kk) koff[kk] = ((2 * kk + h) ^ ((frow >> 1) & 7)) * 16;
+
+  const int pro = min(S - 1, KT);
+  for (int t = 0; t < pro; ++t) issue(t, t);
+  for (int kt = 0; kt < KT; ++kt) {
+    conv_wait<LPT>(min(KT, kt + S - 1) - (kt + 1));
+    lds_barrier();
+    if (kt + S - 1 < KT) issue(kt + S - 1, (kt + S - 1) % S);
+    const char* base = smem + (kt % S) * STAGE;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const bf16x8 fa = *reinterpret_cast<const bf16x8*>(base + arow + koff[kk]);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const bf16x8 fw = *reinterpret_cast<const bf16x8*>(&sB[cur][32 * j + frow][16 * ks + fk]);
+        const bf16x8 fw = *reinterpret_cast<const bf16x8*>(base + brow + j * 32 * ROWB + koff[kk]);
         acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw, fa, acc[j], 0, 0, 0);
       }
     }
-    if (kt + 1 < KT) store(cur ^ 1);
-    __syncthreads();
   }
 
   // epilogue: lane holds pixel m0 + 32 wave + (lane & 31), channels
   // n0 + 32 j + 8 g + 4 (lane >> 5) + 0..3 in acc[j][4 g .. 4 g + 3]
   const int m = m0 + 32 * wave + frow;
   if (m >= M) return;
-  float* orow = p.out + (size_t)m * p.C_out;
+  float* orow = splits > 1 ? p.partial + ((size_t)split * M + m) * p.C_out : p.out + (size_t)m * p.C_out;
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int co = n0 + 32 * j + 8 * g + 4 * (lane >> 5);
-      const float4 b = *reinterpret_cast<const float4*>(p.bias + co);
+      const int co = n0 + 32 * j + 8 * g + 4 * h;
+      float4 b = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (splits == 1) b = *reinterpret_cast<const float4*>(p.bias + co);
       float4 o;
       o.x = acc[j][4 * g + 0] + b.x;
       o.y = acc[j][4 * g + 1] + b.y;
@@ -220,33 +287,75 @@ __global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p) {
     }
 }
 
+// The split launch's partial sums, added in split order, plus the bias.
+__global__ __launch_bounds__(256) void conv_split_reduce_kernel(UNetConvParams p, int splits) {
+  const size_t n4 = (size_t)(p.row_end - p.row_begin) * p.W * p.C_out / 4;
+  const int q4 = p.C_out / 4;
+  const float4* part = reinterpret_cast<const float4*>(p.partial);
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) {
+    float4 v = reinterpret_cast<const float4*>(p.bias)[i % q4];
+    for (int sp = 0; sp < splits; ++sp) {
+      const float4 a = part[(size_t)sp * n4 + i];
+      v.x += a.x; v.y += a.y; v.z += a.z; v.w += a.w;
+    }
+    reinterpret_cast<float4*>(p.out)[i] = v;
+  }
+}
+
 // ---------------------------------------------------------------------------
-size_t unet_conv_workspace_bytes(int W, int C, int G, int rows) {
-  auto al = [](size_t b) { return (b + 255) / 256 * 256; };
-  return al((size_t)rows * G * 2 * sizeof(float)) + al((size_t)G * 2 * sizeof(float)) +
-         al((size_t)rows * W * C * sizeof(bf16));
+static int conv_splits(int M, int C_out) {
+  const int tiles = ceil_div(M, conv::BM) * (C_out / conv::BN);
+  return tiles <= 128 ? conv::SPLITS : 1;
+}
+
+static size_t al256(size_t b) { return (b + 255) / 256 * 256; }
+
+size_t unet_conv_workspace_bytes(int W, int C, int G, int C_out, int rows) {
+  const int M = rows * W;
+  const int sp = conv_splits(M, C_out);
+  return al256((size_t)rows * G * 2 * sizeof(float)) + al256((size_t)G * 2 * sizeof(float)) +
+         al256((size_t)rows * W * C * sizeof(bf16)) + 256 /* zero page */ +
+         (sp > 1 ? al256((size_t)sp * M * C_out * sizeof(float)) : 0);
 }
 
 hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   UNetConvParams p = p0;
   const int rows = p.row_end - p.row_begin;
-  auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+  const int M = rows * p.W;
+  const int sp = conv_splits(M, p.C_out);
   char* w = reinterpret_cast<char*>(ws);
   p.fresh_sums = reinterpret_cast<float*>(w);
-  w += al((size_t)rows * p.G * 2 * sizeof(float));
+  w += al256((size_t)rows * p.G * 2 * sizeof(float));
   p.stats = reinterpret_cast<float*>(w);
-  w += al((size_t)p.G * 2 * sizeof(float));
+  w += al256((size_t)p.G * 2 * sizeof(float));
+  void* act_ws = w;
+  w += al256((size_t)rows * p.W * p.C * sizeof(bf16));
+  p.zero_page = w;
+  w += 256;
+  p.partial = sp > 1 ? reinterpret_cast<float*>(w) : nullptr;
   // the band's activations: straight into the buffer's band rows on a refresh
   p.act_band = p.refresh ? reinterpret_cast<char*>(p.stale_act) + (size_t)p.row_begin * p.W * p.C * sizeof(bf16)
-                         : reinterpret_cast<void*>(w);
-  const int q4 = p.C / 4, shares = q4 <= 256 ? 256 / q4 : 1;
-  hipLaunchKernelGGL(gn_row_sums_kernel, dim3(rows), dim3(256), (size_t)shares * 2 * p.C * sizeof(float), s, p);
+                         : act_ws;
+  const int q4 = p.C / 4, shares = q4 <= kRowSumThreads ? kRowSumThreads / q4 : 1;
+  hipLaunchKernelGGL(gn_row_sums_kernel, dim3(rows), dim3(kRowSumThreads),
+                     (size_t)shares * 2 * p.C * sizeof(float), s, p);
   hipLaunchKernelGGL(gn_stats_kernel, dim3(1), dim3(256), 0, s, p);
   const size_t n4 = (size_t)rows * p.W * p.C / 4;
   const int blocks = (int)std::min<size_t>((n4 + 255) / 256, 4096);
   hipLaunchKernelGGL(gn_silu_kernel, dim3(blocks), dim3(256), 0, s, p);
-  dim3 grid(ceil_div(rows * p.W, conv::BM), p.C_out / conv::BN);
-  hipLaunchKernelGGL(conv3x3_mfma_kernel, grid, dim3(256), 0, s, p);
+  static bool attr = [] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(conv3x3_mfma_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, conv::S * conv::STAGE);
+    return true;
+  }();
+  (void)attr;
+  const int tiles = ceil_div(M, conv::BM) * (p.C_out / conv::BN);
+  hipLaunchKernelGGL(conv3x3_mfma_kernel, dim3(tiles * sp), dim3(256), conv::S * conv::STAGE, s, p, sp);
+  if (sp > 1) {
+    const size_t o4 = (size_t)M * p.C_out / 4;
+    hipLaunchKernelGGL(conv_split_reduce_kernel, dim3((int)std::min<size_t>((o4 + 255) / 256, 4096)),
+                       dim3(256), 0, s, p, sp);
+  }
   return hipGetLastError();
 }
 

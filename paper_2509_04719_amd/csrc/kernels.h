@@ -147,8 +147,10 @@ struct UNetConvParams {
   float* fresh_sums;          // fp32 [rows][G][2]
   float* stats;               // fp32 [G][2]: mean, 1/sqrt(var + eps)
   void* act_band;             // bf16 [rows][W][C]
+  void* zero_page;            // 256 zero bytes (taps outside the map)
+  float* partial;             // split launch: fp32 [splits][rows * W][C_out]
 };
-size_t unet_conv_workspace_bytes(int W, int C, int G, int rows);
+size_t unet_conv_workspace_bytes(int W, int C, int G, int C_out, int rows);
 hipError_t launch_unet_conv(const UNetConvParams& p, void* workspace, hipStream_t stream);
 
 }  // namespace orch

@@ -980,7 +980,7 @@ namespace {
 int check_unet_shape(const orch_unet_conv_shape* s) {
   if (!s) return fail(ORCH_EINVAL, "shape is NULL");
   if (s->height < 1 || s->width < 1) return fail(ORCH_EINVAL, "height and width must be >= 1");
-  if (s->channels < 32 || s->channels % 32) return fail(ORCH_EINVAL, "channels must be a positive multiple of 32");
+  if (s->channels < 64 || s->channels % 64) return fail(ORCH_EINVAL, "channels must be a positive multiple of 64");
   if (s->groups < 1 || s->groups > 256 || s->channels % s->groups)
     return fail(ORCH_EINVAL, "groups must divide channels and be <= 256");
   if (s->out_channels < 64 || s->out_channels % 64) return fail(ORCH_EINVAL, "out_channels must be a positive multiple of 64");
@@ -991,7 +991,7 @@ int check_unet_shape(const orch_unet_conv_shape* s) {
 
 size_t orch_unet_conv_workspace_bytes(const orch_unet_conv_shape* s, int band_rows) {
   if (!s || band_rows < 1 || s->groups < 1 || s->channels < 1) return 0;
-  return unet_conv_workspace_bytes(s->width, s->channels, s->groups, band_rows);
+  return unet_conv_workspace_bytes(s->width, s->channels, s->groups, s->out_channels, band_rows);
 }
 
 int orch_unet_conv_band(const orch_unet_conv_shape* s, int rb, int re, const float* x_band,
@@ -1008,7 +1008,7 @@ int orch_unet_conv_band(const orch_unet_conv_shape* s, int rb, int re, const flo
   if ((!all_rows || refresh) && (!stale_act || !stale_sums))
     return fail(ORCH_EINVAL, "stale_act and stale_sums are needed unless the band is every row without refresh");
   const int rows = re - rb;
-  const size_t need = unet_conv_workspace_bytes(s->width, s->channels, s->groups, rows);
+  const size_t need = unet_conv_workspace_bytes(s->width, s->channels, s->groups, s->out_channels, rows);
   if (workspace_bytes < need) return fail(ORCH_EINVAL, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   if (((uintptr_t)x_band | (uintptr_t)gamma | (uintptr_t)beta | (uintptr_t)weight | (uintptr_t)bias |
        (uintptr_t)stale_act | (uintptr_t)stale_sums | (uintptr_t)out | (uintptr_t)workspace) & 15)

@@ -97,7 +97,10 @@ def test_unet_sdxl_stage1(orch_lib, rb, re, refresh):
 def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
     """The all-rows pass with refresh fills both buffers; bands then read
     their halo rows and the other rows' sums from them, and stitch to the
-    all-rows output bit for bit (every output's sum runs in the same order)."""
+    all-rows output bit for bit (every output's sum runs in the same order).
+    Bands of 26 rows and more run the convolution unsplit, as the all-rows
+    pass does; shorter ones split the taps over more workgroups and add the
+    partial sums in another order, equal up to rounding."""
     cfg, pr, _, x, _, _ = _setup("unet_sdxl_1024_stage1")
     H, W, C, Co, G = cfg.height, cfg.width, cfg.channels, cfg.out_channels, cfg.groups
     shape = orch_lib.unet_shape(cfg, EPS)
@@ -110,15 +113,18 @@ def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
     full = torch.empty((H, W, Co), device=DEV)
     orch_lib.unet_conv_band(shape, 0, H, xd, dev["gamma"], dev["beta"], wt, dev["bias"], act, sums,
                             1, full, ws)
-    stitched = torch.empty_like(full)
-    for rb, re in [(0, 16), (16, 72), (72, 73), (73, 128)]:
-        o = torch.empty((re - rb, W, Co), device=DEV)
-        orch_lib.unet_conv_band(shape, rb, re, xd[rb:re].contiguous(), dev["gamma"], dev["beta"],
-                                wt, dev["bias"], act, sums, 0, o, ws)
-        stitched[rb:re] = o
-    torch.cuda.synchronize()
+    def stitch(cuts):
+        out = torch.empty_like(full)
+        for rb, re in zip(cuts[:-1], cuts[1:]):
+            o = torch.empty((re - rb, W, Co), device=DEV)
+            orch_lib.unet_conv_band(shape, rb, re, xd[rb:re].contiguous(), dev["gamma"], dev["beta"],
+                                    wt, dev["bias"], act, sums, 0, o, ws)
+            out[rb:re] = o
+        torch.cuda.synchronize()
+        return out
     assert not torch.isnan(full).any()
-    assert torch.equal(stitched, full)
+    assert torch.equal(stitch([0, 40, 72, 128]), full)
+    assert rel_l2(to_host(stitch([0, 16, 72, 73, 128])), to_host(full)) <= 1e-6
 
 
 def test_unet_rejects_bad_arguments(orch_lib):
@@ -132,7 +138,7 @@ def test_unet_rejects_bad_arguments(orch_lib):
     with pytest.raises(orch_lib.OrchError) as e:
         orch_lib.unet_conv_band(shape, 2, 6, t, t, t, t, t, None, None, 0, t[:100], ws)
     assert "stale" in str(e.value)
-    bad = orch_lib.UNetConvShape(16, 16, 48, 8, 64, EPS)
+    bad = orch_lib.UNetConvShape(16, 16, 96, 8, 64, EPS)
     with pytest.raises(orch_lib.OrchError) as e:
         orch_lib.unet_conv_band(bad, 0, 4, t, t, t, t, t, t, t, 0, t[:100], ws)
-    assert "multiple of 32" in str(e.value)
+    assert "multiple of 64" in str(e.value)
