@@ -17,7 +17,9 @@
 // padded (d = 72 -> 80 rows of O^T), one padding row of V^T holds ones, so
 // the PV product also accumulates the softmax denominator.  exp2 runs on
 // v_exp_f32 with log2(e)/sqrt(d) folded into the exponent; the running max is
-// raised lazily (only past a 2^8 margin), so O is rarely rescaled.  The loop
+// set with headroom and raised lazily, tested after the exponentials by one
+// bit of the packed bf16 probabilities, so O is rarely rescaled and no max is
+// taken on the common path.  The loop
 // runs over 32-key halves of a tile: the MFMAs of the next half's scores are
 // issued between the current half's exponentials, then its PV MFMAs.  Built
 // without IEEE NaN quieting, so the row max is plain v_max3_f32.
@@ -34,6 +36,10 @@ namespace mfma_attn {
 // and slower where the query count is not a multiple of 256.)
 constexpr int BQ = 128, BKV = 64, NSTAGE = 4;
 constexpr int NW = BQ / 32, KW = NW / 2, NTHR = 64 * NW, WPC = 512 / NTHR;
+// headroom of the running max: a raise puts it this far above the largest
+// score so far, and the next raise comes when a score exceeds it by one, so
+// the running max moves rarely (about once per 8 of score growth, log2 units)
+constexpr float kLead = 7.0f;
 
 template <int D>
 struct Geo {
@@ -320,6 +326,23 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
     pp[1] = __builtin_bit_cast(bf16x8, q1);
   };
 
+  // the largest of a query's 32 scores (its two lane halves)
+  auto query_max = [&](const f32x16& v) {
+    float mx = fmaxf(fmaxf(v[0], v[1]), v[2]);
+#pragma unroll
+    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, v[r]), v[r + 1]);
+    return max_xhalf(fmaxf(mx, v[15]));
+  };
+  // -m_run into the score chains' input (max column or accumulator)
+  auto m_changed = [&]() {
+    if constexpr (G::MCOL) {
+      set_mcol();
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) negm[r] = -m_run;
+    }
+  };
+
   // One 32-key half of the stream of key tiles.  sc: S^T of keys [32 sub,
   // +32) of the tile in stage st.  Its exponentials are interleaved with the
   // MFMAs of the next half's scores (NEXT: K fragments of stage nst, half
@@ -333,52 +356,26 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
     // and every score chain subtracts m_run (through the max column, else as
     // the accumulator input), so sc holds s - m_run and the probability is
     // exp2(sc) with nothing in between.
-    // The running max m_run is a whole number, set on a segment's first half
-    // and raised only when some lane's max exceeds it by more than 8: until
-    // then exp2(sc) <= 2^8, exact in fp32 and in range for bf16, so O is
-    // rarely rescaled; when it is, by a power of two, which scales the
-    // previous half's pending probabilities exactly too.  The fragment reads
-    // go first, in order of use; the lane swaps and the max below cover their
-    // latency.
+    // The running max m_run is a whole number: a segment's first half sets it
+    // kLead above its largest score; later halves compute their probabilities
+    // first and test them afterwards with one bit (any probability >= 2), so
+    // no max is taken while the probabilities stay below 2.  When one reaches
+    // 2, the half's scores are lowered by a whole d (to kLead below the new
+    // max), its probabilities recomputed and O scaled by 2^-d.  The fragment
+    // reads go first, in order of use; the lane swaps cover their latency.
     bf16x8 vp[NT];
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) vp[tt] = v_frag(pst, tt, psub);
     bf16x8 kn[NC];
     if constexpr (NEXT) k_frags(nst, nsub, kn);
     p_swap(pp);   // pp[j]: queries 16 j .. +16
-    // a chain of three-way maxima (v_max3_f32: two new values each)
-    float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
-#pragma unroll
-    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sc[r]), sc[r + 1]);
-    mx = fmaxf(mx, sc[15]);
-    mx = max_xhalf(mx);   // VALU swap: no LDS round trip behind the fragment reads
-    float alpha = 1.0f;
-    if (__builtin_expect(__any(start || mx > 8.0f), 0)) {
-      // raise (or, on a segment's first half, set) the max by a whole d
-      const float d = (start || mx > 8.0f) ? ceilf(mx) : 0.0f;
-      alpha = start ? 1.0f : ldexpf(1.0f, -(int)fminf(d, 160.0f));
-      m_run += d;
+    if (start) {
+      // m_run is zero here, O and the pending probabilities too
+      const float d = ceilf(query_max(sc)) + kLead;
+      m_run = d;
 #pragma unroll
       for (int r = 0; r < 16; ++r) sc[r] -= d;
-      if constexpr (G::MCOL) {
-        set_mcol();
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) negm[r] = -m_run;
-      }
-      // O^T and the swapped probabilities hold queries 16 j + (lane & 15)
-      float aj[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) aj[j] = __shfl(alpha, 16 * j + r16, kWave);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) oo[(2 * tt + j) / 4][4 * ((2 * tt + j) % 4) + r] *= aj[j];   // oget(tt, j) *= aj[j]
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pp[j][e] = (bf16)((float)pp[j][e] * aj[j]);
-      }
+      m_changed();
     }
     __builtin_amdgcn_sched_barrier(0);
     // the MFMA-dense part runs at raised wave priority: the two waves sharing a
@@ -420,6 +417,47 @@ __global__ __launch_bounds__(mfma_attn::NTHR, mfma_attn::WPC) void attn_bf16_mfm
       asm volatile("" ::"v"(pc[ci]));
     });
     __builtin_amdgcn_s_setprio(0);
+    // any probability >= 2 (or not finite): bf16 exponent bit 7 set
+    float alpha = 1.0f;
+    {
+      typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+      const u32x4 a = __builtin_bit_cast(u32x4, pc[0]), b = __builtin_bit_cast(u32x4, pc[1]);
+      const unsigned w = a[0] | a[1] | a[2] | a[3] | b[0] | b[1] | b[2] | b[3];
+      if (__builtin_expect(__any((w & 0x40004000u) != 0u), 0)) {
+        const float mx = query_max(sc);
+        const float d = mx >= 1.0f ? ceilf(mx) + kLead : 0.0f;
+        alpha = ldexpf(1.0f, -(int)fminf(d, 160.0f));
+        m_run += d;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] -= d;
+        // the next half's scores were formed with the old m_run
+        if constexpr (NEXT) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sn[r] -= d;
+        }
+        m_changed();
+        psum = 0.0f;
+#pragma unroll
+        for (int ci = 0; ci < 2; ++ci)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pv_ = __builtin_amdgcn_exp2f(sc[4 * (2 * ci + (e >> 2)) + (e & 3)]);
+            if constexpr (!G::ONES) psum += pv_;
+            pc[ci][e] = (bf16)pv_;
+          }
+        // O^T holds queries 16 j + (lane & 15); its PV products so far used
+        // the old m_run
+        float aj[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) aj[j] = __shfl(alpha, 16 * j + r16, kWave);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) oo[(2 * tt + j) / 4][4 * ((2 * tt + j) % 4) + r] *= aj[j];   // oget(tt, j) *= aj[j]
+      }
+    }
     if constexpr (!G::ONES) l_run = l_run * alpha + psum;
   };
 

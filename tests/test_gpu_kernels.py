@@ -212,11 +212,14 @@ def test_qkv_scatter_every_tile(orch_lib, force_tile, tile):
 # ---- attention over fresh + stale K/V --------------------------------------
 
 def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fresh, seed,
-                    sample_rows=None, split=True, k_ramp=0.0, shift=0.0):
+                    sample_rows=None, split=True, k_ramp=0.0, shift=0.0, k_spike=0.0):
     """k_ramp: key j's vector scaled by 1 + k_ramp j / n_kv (scores grow along
     the key stream, so the running max moves mid-stream); shift: the first
     channel of every head set to `shift` in Q and K (every score of a query
-    raised by the same large amount: softmax unchanged, running max large)."""
+    raised by the same large amount: softmax unchanged, running max large);
+    k_spike: the 32 keys from n_kv / 2 on score k_spike-proportionally higher
+    (a jump of over 127 in log2 units mid-stream: exp2 of the scores overflows
+    before the running max is raised)."""
     H = heads * d
     R = int(np.sqrt(n_kv))
     hdr = {"hidden": H, "heads": heads, "grid": R}
@@ -233,6 +236,16 @@ def _attention_case(orch_lib, dtype, B, heads, d, n_q, n_kv, fresh_begin, n_fres
     if shift:
         for arr in (q, Ks, Kf):
             arr[:, :, 0::d] = shift
+    if k_spike:
+        # channel 1 of every head: 16 in Q, k_spike in the 32 spiked keys, so
+        # their scores share an offset of 16 k_spike / sqrt(d) (the offset's
+        # rounding cancels in the softmax over them; the others vanish)
+        j0 = n_kv // 2
+        q[:, :, 1::d] = 16.0
+        Ks[:, j0:j0 + 32, 1::d] = k_spike
+        f0, f1 = max(j0 - fresh_begin, 0), min(j0 + 32 - fresh_begin, Kf.shape[1])
+        if n_fresh and f0 < f1:
+            Kf[:, f0:f1, 1::d] = k_spike
     qd = to_dev(np.stack([q[b].reshape(n_q, heads, d).transpose(1, 0, 2) for b in range(B)]), dtype)
     stale = np.concatenate([dit.kv_to_buffer_layout(hdr, Ks[b], Vs[b]) for b in range(B)])
     fresh = np.concatenate([dit.kv_to_buffer_layout(hdr, Kf[b], Vf[b]) for b in range(B)])
@@ -286,8 +299,9 @@ def test_attention_split_keys(orch_lib, split, d, n_q, n_kv, fb, nf):
 @pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("d,n_q,n_kv,fb,nf", [(72, 384, 1024, 256, 384), (64, 1664, 2304, 256, 1664),
                                              (72, 1664, 4096, 0, 1664)])
-@pytest.mark.parametrize("k_ramp,shift", [(12.0, 0.0), (0.0, 48.0), (12.0, 48.0)])
-def test_attention_running_max(orch_lib, split, d, n_q, n_kv, fb, nf, k_ramp, shift):
+@pytest.mark.parametrize("k_ramp,shift,k_spike", [(12.0, 0.0, 0.0), (0.0, 48.0, 0.0), (12.0, 48.0, 0.0),
+                                                  (0.0, 0.0, 64.0)])
+def test_attention_running_max(orch_lib, split, d, n_q, n_kv, fb, nf, k_ramp, shift, k_spike):
     """The lazy running max: scores growing along the key stream (the max is
     raised and O rescaled mid-stream, also in the pending probabilities of
     the lagging PV product), and a large common score offset (a running max
@@ -295,7 +309,7 @@ def test_attention_running_max(orch_lib, split, d, n_q, n_kv, fb, nf, k_ramp, sh
     column).  Sampled query rows at the large shapes."""
     rows = np.r_[np.arange(0, n_q, 37), n_q - 1] if n_q > 1000 else None
     err = _attention_case(orch_lib, "bf16", 2, 16, d, n_q, n_kv, fb, nf, seed=n_q + d + 7, split=split,
-                          sample_rows=rows, k_ramp=k_ramp, shift=shift)
+                          sample_rows=rows, k_ramp=k_ramp, shift=shift, k_spike=k_spike)
     assert err <= 1e-2, err
 
 
