@@ -477,39 +477,47 @@ def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
 
 def run_unet(a) -> int:
     """The U-Net band block (GroupNorm -> SiLU -> conv3x3 with stale halo rows
-    and stale group statistics) on SDXL's first stage at 1024px: ms per call
-    and the convolution's TFLOP/s per band."""
+    and stale group statistics) on the three stages of an SDXL-sized U-Net at
+    1024px (128 x 128 x 320, 64 x 64 x 640, 32 x 32 x 1280): ms per call and
+    the convolution's TFLOP/s per band (an interior 1/8, the 14/32 head, the
+    18/32 tail and every row)."""
     import numpy as np
     import torch
 
     from paper_2509_04719_amd import _lib as L
     from seeded_inputs import configs, generate
 
-    cfg = configs.UNET_SDXL_1024
     dev = "cuda:0"
-    H, W, C, Co, G = cfg.height, cfg.width, cfg.channels, cfg.out_channels, cfg.groups
-    shape = L.unet_shape(cfg)
-    pr = generate.make_unet_params(cfg, 0)
-    x = torch.from_numpy(generate.make_unet_input(cfg, 0)).to(dev)
-    gamma, beta, bias = (torch.from_numpy(pr[k]).to(dev) for k in ("gamma", "beta", "bias"))
-    wt = torch.from_numpy(pr["weight_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
-    act = torch.zeros((H, W, C), dtype=torch.bfloat16, device=dev)
-    sums = torch.zeros((H, G, 2), device=dev)
-    ws = torch.empty(L.unet_conv_workspace_bytes(shape, H), dtype=torch.uint8, device=dev)
-    full = torch.empty((H, W, Co), device=dev)
-    L.unet_conv_band(shape, 0, H, x, gamma, beta, wt, bias, act, sums, 1, full, ws)   # fill buffers
-    res = {}
-    for rb, re in [(56, 72), (0, 56), (56, 128), (0, H)]:
-        r = re - rb
-        xb = x[rb:re].contiguous()
-        o = torch.empty((r, W, Co), device=dev)
-        ms = _time_loop(torch, lambda: L.unet_conv_band(shape, rb, re, xb, gamma, beta, wt, bias, act,
-                                                        sums, 1, o, ws), a.steps)
-        fl = 2.0 * r * W * Co * 9 * C
-        res[f"[{rb},{re})"] = {"rows": r, "ms": round(ms, 4), "conv_tflops": round(fl / ms / 1e9, 1)}
-    out = {"metric": "U-Net band block ms (GroupNorm, SiLU, conv3x3), SDXL stage 1 at 1024px",
-           "unit": "ms", "config": {"workload": f"{cfg.name}: {H}x{W}x{C}, {G} groups -> {Co}"},
-           "bands": res}
+    stages = {}
+    for cfg in (configs.UNET_SDXL_1024, configs.UNET_SDXL_1024_S2, configs.UNET_SDXL_1024_S3):
+        H, W, C, Co, G = cfg.height, cfg.width, cfg.channels, cfg.out_channels, cfg.groups
+        shape = L.unet_shape(cfg)
+        pr = generate.make_unet_params(cfg, 0)
+        x = torch.from_numpy(generate.make_unet_input(cfg, 0)).to(dev)
+        gamma, beta, bias = (torch.from_numpy(pr[k]).to(dev) for k in ("gamma", "beta", "bias"))
+        wt = torch.from_numpy(pr["weight_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+        act = torch.zeros((H, W, C), dtype=torch.bfloat16, device=dev)
+        sums = torch.zeros((H, G, 2), device=dev)
+        bands = [(7 * H // 16, 9 * H // 16), (0, 14 * H // 32), (14 * H // 32, H), (0, H)]
+        # short bands split the taps over more workgroups (fp32 partials): the
+        # workspace is sized for every band height used
+        wsb = max(L.unet_conv_workspace_bytes(shape, re - rb) for rb, re in bands)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        full = torch.empty((H, W, Co), device=dev)
+        L.unet_conv_band(shape, 0, H, x, gamma, beta, wt, bias, act, sums, 1, full, ws)   # fill buffers
+        res = {}
+        for rb, re in bands:
+            r = re - rb
+            xb = x[rb:re].contiguous()
+            o = torch.empty((r, W, Co), device=dev)
+            ms = _time_loop(torch, lambda: L.unet_conv_band(shape, rb, re, xb, gamma, beta, wt, bias,
+                                                            act, sums, 1, o, ws), a.steps)
+            fl = 2.0 * r * W * Co * 9 * C
+            res[f"[{rb},{re})"] = {"rows": r, "ms": round(ms, 4), "conv_tflops": round(fl / ms / 1e9, 1)}
+        stages[cfg.name] = {"shape": f"{H}x{W}x{C}, {G} groups -> {Co}", "bands": res}
+        del x, wt, act, sums, ws, full
+    out = {"metric": "U-Net band block ms (GroupNorm, SiLU, conv3x3), SDXL-sized stages at 1024px",
+           "unit": "ms", "stages": stages}
     print(json.dumps(out), flush=True)
     return 0
 

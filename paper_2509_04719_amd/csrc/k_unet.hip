@@ -157,7 +157,6 @@ constexpr int STAGE = (BM + BN) * ROWB;              // 24 KB
 constexpr int LA = BM * ROWB / (NW * 1024);          // A loads per lane per k-tile (4)
 constexpr int LB = BN * ROWB / (NW * 1024);          // B loads per lane per k-tile (2)
 constexpr int LPT = LA + LB;
-constexpr int SPLITS = 3;                            // tap groups of a split launch
 }
 
 template <int LPTn>
@@ -303,9 +302,14 @@ __global__ __launch_bounds__(256) void conv_split_reduce_kernel(UNetConvParams p
 }
 
 // ---------------------------------------------------------------------------
+// Tap groups of a launch (1, 3 or 9: one per kernel row or per tap): the
+// most that still run in one round of two workgroups per CU, so short bands
+// and deep stages (few pixels, many channels) fill the machine.
 static int conv_splits(int M, int C_out) {
   const int tiles = ceil_div(M, conv::BM) * (C_out / conv::BN);
-  return tiles <= 128 ? conv::SPLITS : 1;
+  for (const int s : {9, 3})
+    if (tiles * s <= 2 * 256) return s;
+  return 1;
 }
 
 static size_t al256(size_t b) { return (b + 255) / 256 * 256; }

@@ -165,4 +165,14 @@ UNET_SDXL_1024 = UNetConvConfig(name="unet_sdxl_1024_stage1", height=128, width=
                                 channels=320, groups=32, out_channels=320,
                                 band_rows=(16, 56, 72), share_labels=("1/8", "14/32", "18/32"))
 
-UNET_CONFIGS = (UNET_TINY, UNET_SDXL_1024)
+# The deeper stages of the same U-Net at 1024px: 64 x 64 with 640 channels
+# and 32 x 32 with 1280 channels, 32 groups each; bands at the same shares of
+# the rows (1/8 in the interior, 14/32 at the head, 18/32 at the tail).
+UNET_SDXL_1024_S2 = UNetConvConfig(name="unet_sdxl_1024_stage2", height=64, width=64,
+                                   channels=640, groups=32, out_channels=640,
+                                   band_rows=(8, 28, 36), share_labels=("1/8", "14/32", "18/32"))
+UNET_SDXL_1024_S3 = UNetConvConfig(name="unet_sdxl_1024_stage3", height=32, width=32,
+                                   channels=1280, groups=32, out_channels=1280,
+                                   band_rows=(4, 14, 18), share_labels=("1/8", "14/32", "18/32"))
+
+UNET_CONFIGS = (UNET_TINY, UNET_SDXL_1024, UNET_SDXL_1024_S2, UNET_SDXL_1024_S3)

@@ -94,13 +94,24 @@ def test_unet_sdxl_stage1(orch_lib, rb, re, refresh):
     _run(orch_lib, "unet_sdxl_1024_stage1", rb, re, refresh)
 
 
+# the deeper stages: 64 x 64 x 640 and 32 x 32 x 1280 (bands at the same shares)
+@pytest.mark.parametrize("name,rows", [("unet_sdxl_1024_stage2", 64), ("unet_sdxl_1024_stage3", 32)],
+                         ids=["stage2", "stage3"])
+@pytest.mark.parametrize("share", ["1/8", "14/32", "18/32", "all"])
+def test_unet_sdxl_deeper_stages(orch_lib, name, rows, share):
+    rb, re, refresh = {"1/8": (7 * rows // 16, 9 * rows // 16, 1), "14/32": (0, 14 * rows // 32, 0),
+                       "18/32": (14 * rows // 32, rows, 1), "all": (0, rows, 1)}[share]
+    _run(orch_lib, name, rb, re, refresh)
+
+
 def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
     """The all-rows pass with refresh fills both buffers; bands then read
     their halo rows and the other rows' sums from them, and stitch to the
     all-rows output bit for bit (every output's sum runs in the same order).
-    Bands of 26 rows and more run the convolution unsplit, as the all-rows
-    pass does; shorter ones split the taps over more workgroups and add the
-    partial sums in another order, equal up to rounding."""
+    Bands of 35 rows and more run the convolution unsplit, as the all-rows
+    pass does; shorter ones split the taps over more workgroups (3 groups
+    from 34 rows down, 9 from 11) and add the partial sums in another order,
+    equal up to rounding."""
     cfg, pr, _, x, _, _ = _setup("unet_sdxl_1024_stage1")
     H, W, C, Co, G = cfg.height, cfg.width, cfg.channels, cfg.out_channels, cfg.groups
     shape = orch_lib.unet_shape(cfg, EPS)
@@ -109,7 +120,10 @@ def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
     xd = torch.from_numpy(x).to(DEV)
     act = torch.full((H, W, C), float("nan"), dtype=torch.bfloat16, device=DEV)
     sums = torch.full((H, G, 2), float("nan"), device=DEV)
-    ws = torch.empty(orch_lib.unet_conv_workspace_bytes(shape, H), dtype=torch.uint8, device=DEV)
+    cuts_exact, cuts_split = [0, 40, 76, 128], [0, 16, 72, 73, 128]
+    heights = {H} | {b - a for cuts in (cuts_exact, cuts_split) for a, b in zip(cuts[:-1], cuts[1:])}
+    ws = torch.empty(max(orch_lib.unet_conv_workspace_bytes(shape, r) for r in heights), dtype=torch.uint8,
+                     device=DEV)
     full = torch.empty((H, W, Co), device=DEV)
     orch_lib.unet_conv_band(shape, 0, H, xd, dev["gamma"], dev["beta"], wt, dev["bias"], act, sums,
                             1, full, ws)
@@ -123,8 +137,8 @@ def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
         torch.cuda.synchronize()
         return out
     assert not torch.isnan(full).any()
-    assert torch.equal(stitch([0, 40, 72, 128]), full)
-    assert rel_l2(to_host(stitch([0, 16, 72, 73, 128])), to_host(full)) <= 1e-6
+    assert torch.equal(stitch(cuts_exact), full)
+    assert rel_l2(to_host(stitch(cuts_split)), to_host(full)) <= 1e-6
 
 
 def test_unet_rejects_bad_arguments(orch_lib):
