@@ -59,14 +59,21 @@ __global__ __launch_bounds__(kRowSumThreads) void gn_row_sums_kernel(UNetConvPar
     }
   }
   __syncthreads();
+  // channel totals over the shares (in share order) into share 0's slots,
+  // then group totals over the channels (in channel order)
+  for (int i = threadIdx.x; i < 2 * C; i += kRowSumThreads) {
+    float a = s_part[i];
+    for (int k = 1; k < per; ++k) a += s_part[(size_t)k * 2 * C + i];
+    s_part[i] = a;
+  }
+  __syncthreads();
   const int cg = C / p.G;
   for (int g = threadIdx.x; g < p.G; g += kRowSumThreads) {
     float a = 0.0f, b = 0.0f;
-    for (int c = g * cg; c < (g + 1) * cg; ++c)
-      for (int k = 0; k < per; ++k) {
-        a += s_part[(size_t)k * 2 * C + 2 * c];
-        b += s_part[(size_t)k * 2 * C + 2 * c + 1];
-      }
+    for (int c = g * cg; c < (g + 1) * cg; ++c) {
+      a += s_part[2 * c];
+      b += s_part[2 * c + 1];
+    }
     float2 v = make_float2(a, b);
     reinterpret_cast<float2*>(p.fresh_sums)[(size_t)y * p.G + g] = v;
     if (p.refresh) reinterpret_cast<float2*>(p.stale_sums)[(size_t)(p.row_begin + y) * p.G + g] = v;
