@@ -516,10 +516,50 @@ def run_unet(a) -> int:
             res[f"[{rb},{re})"] = {"rows": r, "ms": round(ms, 4), "conv_tflops": round(fl / ms / 1e9, 1)}
         stages[cfg.name] = {"shape": f"{H}x{W}x{C}, {G} groups -> {Co}", "bands": res}
         del x, wt, act, sums, ws, full
+    # the dominant kernel is the convolution; its rate here is the convolution's
+    # FLOPs over the whole call (GroupNorm launches included), a lower bound
+    s1 = stages[configs.UNET_SDXL_1024.name]["bands"]
+    full_band = s1[f"[0,{configs.UNET_SDXL_1024.height})"]
+    roofline = {"kernel": "conv3x3_mfma (whole call timed)", "bound": "mfma",
+                "achieved": full_band["conv_tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(full_band["conv_tflops"] / PEAK_BF16_TFLOPS, 4),
+                "workload": f"{configs.UNET_SDXL_1024.name}, every row"}
     out = {"metric": "U-Net band block ms (GroupNorm, SiLU, conv3x3), SDXL-sized stages at 1024px",
-           "unit": "ms", "stages": stages}
+           "unit": "ms", "stages": stages, "roofline": roofline}
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = unet_cpu_baseline(configs.UNET_SDXL_1024, 0, configs.UNET_SDXL_1024.height)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def unet_cpu_baseline(cfg, rb, re):
+    """The oracle (float64 numpy) timed on one U-Net band call: the group
+    statistics from fresh and stale sums, GroupNorm, SiLU, the convolution."""
+    import numpy as np
+
+    from oracle import unet
+    from oracle.blob import bf16_to_float
+    from seeded_inputs import generate
+    pr = generate.make_unet_params(cfg, 0)
+    params = {"gamma": pr["gamma"].astype(np.float64), "beta": pr["beta"].astype(np.float64),
+              "weight": bf16_to_float(pr["weight_bits"]).astype(np.float64),
+              "bias": pr["bias"].astype(np.float64)}
+    x = generate.make_unet_input(cfg, 0).astype(np.float64)
+    stale_act = np.zeros((cfg.height, cfg.width, cfg.channels))
+    stale_sums = np.ones((cfg.height, cfg.groups, 2))
+    times = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        unet.band_step(params, x[rb:re], cfg.height, rb, re, cfg.groups, stale_act, stale_sums, 1e-5)
+        times.append(time.perf_counter() - t0)
+    dt = sorted(times)[1]
+    fl = 2.0 * (re - rb) * cfg.width * cfg.out_channels * 9 * cfg.channels
+    info = host_info()
+    cores = info["blas_threads"] or info["affinity_cores"]
+    return {"value": round(fl / dt / 1e12, 5), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{cfg.name} band rows [{rb},{re}) ({re - rb}/{cfg.height}), float64 numpy: "
+                      f"median of three calls of {fl / 1e9:.2f} GFLOP (convolution), {dt:.2f} s each",
+            "ms_per_call": round(dt * 1e3, 1), **info}
 
 
 def main(argv=None) -> int:

@@ -310,12 +310,14 @@ __global__ __launch_bounds__(256) void conv_split_reduce_kernel(UNetConvParams p
 
 // ---------------------------------------------------------------------------
 // Tap groups of a launch (1, 3 or 9: one per kernel row or per tap): the
-// most that still run in one round of two workgroups per CU, so short bands
-// and deep stages (few pixels, many channels) fill the machine.
+// most whose workgroups stay within a quarter over one round of two per CU,
+// so short bands and deep stages (few pixels, many channels) fill the
+// machine with two workgroups per CU (a lone workgroup per CU runs its
+// k-loop much slower).
 static int conv_splits(int M, int C_out) {
   const int tiles = ceil_div(M, conv::BM) * (C_out / conv::BN);
   for (const int s : {9, 3})
-    if (tiles * s <= 2 * 256) return s;
+    if (tiles * s <= 2 * 256 * 5 / 4) return s;
   return 1;
 }
 

@@ -108,9 +108,9 @@ def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
     """The all-rows pass with refresh fills both buffers; bands then read
     their halo rows and the other rows' sums from them, and stitch to the
     all-rows output bit for bit (every output's sum runs in the same order).
-    Bands of 35 rows and more run the convolution unsplit, as the all-rows
+    Bands of 43 rows and more run the convolution unsplit, as the all-rows
     pass does; shorter ones split the taps over more workgroups (3 groups
-    from 34 rows down, 9 from 11) and add the partial sums in another order,
+    from 42 rows down, 9 from 14) and add the partial sums in another order,
     equal up to rounding."""
     cfg, pr, _, x, _, _ = _setup("unet_sdxl_1024_stage1")
     H, W, C, Co, G = cfg.height, cfg.width, cfg.channels, cfg.out_channels, cfg.groups
@@ -120,7 +120,7 @@ def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
     xd = torch.from_numpy(x).to(DEV)
     act = torch.full((H, W, C), float("nan"), dtype=torch.bfloat16, device=DEV)
     sums = torch.full((H, G, 2), float("nan"), device=DEV)
-    cuts_exact, cuts_split = [0, 40, 76, 128], [0, 16, 72, 73, 128]
+    cuts_exact, cuts_split = [0, 56, 128], [0, 16, 40, 72, 73, 128]
     heights = {H} | {b - a for cuts in (cuts_exact, cuts_split) for a, b in zip(cuts[:-1], cuts[1:])}
     ws = torch.empty(max(orch_lib.unet_conv_workspace_bytes(shape, r) for r in heights), dtype=torch.uint8,
                      device=DEV)
