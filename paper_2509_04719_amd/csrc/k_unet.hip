@@ -144,9 +144,10 @@ __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
 
 // ---------------------------------------------------------------------------
 // 4. The convolution as an implicit GEMM.  Workgroup tile: 128 band pixels x
-// 64 output channels, four waves of 32 pixels; k-tiles of one tap x 64 input
-// channels (128-byte rows), loaded straight into LDS (16 bytes per lane, no
-// register staging) into a ring of three stages, one barrier per k-tile.  A
+// 64 output channels, four waves of 32 pixels (or x 128 channels, eight
+// waves, see below); k-tiles of one tap x 64 input channels (128-byte rows),
+// loaded straight into LDS (16 bytes per lane, no register staging) into a
+// ring of stages, one barrier per k-tile.  A
 // lane of a wave-level load fills LDS row (lane / 8) of its 8-row slab at
 // physical chunk lane % 8, holding logical chunk (lane % 8) ^ ((row / 2) % 8):
 // the fragment reads (16 rows at one logical chunk) then hit distinct banks.
@@ -154,30 +155,51 @@ __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
 // read from the band's activations, the stale buffer (halo rows) or a zero
 // page (outside the map).  The MFMAs take the weight rows as the first
 // operand, so a lane ends with four consecutive output channels of one pixel.
-// Short bands split the nine taps in three groups of three (one per kernel
-// row dy) over more workgroups; their fp32 partial sums are added in order by
-// a second kernel, which adds the bias.
+// Launches with few tiles split their k-tiles (tap, channel chunk) in even
+// ranges over more workgroups; the fp32 partial sums are added in order by a
+// second kernel, which adds the bias.  Output widths divisible by 128 take
+// 128-channel tiles on eight waves (one workgroup per CU, four stages).
 namespace conv {
-constexpr int BM = 128, BN = 64, BK = 64, S = 3, NW = 4;
+constexpr int BM = 128, BK = 64;
 constexpr int ROWB = 2 * BK;                         // bytes per LDS row
-constexpr int STAGE = (BM + BN) * ROWB;              // 24 KB
-constexpr int LA = BM * ROWB / (NW * 1024);          // A loads per lane per k-tile (4)
-constexpr int LB = BN * ROWB / (NW * 1024);          // B loads per lane per k-tile (2)
-constexpr int LPT = LA + LB;
+// BN output channels per workgroup over NW waves (each 32 pixels x 64
+// channels), a ring of S stages
+template <int BN_, int NW_, int S_>
+struct Geo {
+  static constexpr int BN = BN_, NW = NW_, S = S_;
+  static constexpr int STAGE = (BM + BN) * ROWB;
+  static constexpr int LA = BM * ROWB / (NW * 1024);  // A loads per lane per k-tile
+  static constexpr int LB = BN * ROWB / (NW * 1024);  // B loads per lane per k-tile
+  static constexpr int LPT = LA + LB;
+  static constexpr int WPC = 160 * 1024 / (S * STAGE);  // workgroups per CU (LDS)
+  static_assert(NW * 64 == 4 * BN, "four waves of 32 pixels per 64 channels");
+  static_assert(LA * NW * 1024 == BM * ROWB && LB * NW * 1024 == BN * ROWB, "whole wave-level loads");
+  static_assert(S >= 2 && S <= 4 && (S - 1) * LPT < 64, "ring depth");
+};
+// 64 channels: 24 KB stages, three, two workgroups of four waves per CU;
+// 128 channels (output widths divisible by 128): 32 KB stages, four, one
+// workgroup of eight waves per CU, a third fewer operand bytes per MAC
+using Narrow = Geo<64, 4, 3>;
+using Wide = Geo<128, 8, 4>;
 }
 
 template <int LPTn>
 __device__ __forceinline__ void conv_wait(int tiles_after) {
-  if (tiles_after >= 2) wait_vmcnt<2 * LPTn>();
+  if (tiles_after >= 3) wait_vmcnt<3 * LPTn>();
+  else if (tiles_after == 2) wait_vmcnt<2 * LPTn>();
   else if (tiles_after == 1) wait_vmcnt<LPTn>();
   else wait_vmcnt<0>();
 }
 
-__global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p, int splits) {
+template <class G>
+__global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams p, int splits) {
   using namespace conv;
+  constexpr int BN = G::BN, NW = G::NW, S = G::S, STAGE = G::STAGE, LA = G::LA, LB = G::LB, LPT = G::LPT;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // wave's 32 pixels (wm) and 64 output channels (wn) of the tile
+  const int wm = wave % 4, wn = wave / 4;
   const int rows = p.row_end - p.row_begin;
   const int M = rows * p.W;
   const int tiles_n = p.C_out / BN;
@@ -187,8 +209,8 @@ __global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p, int
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
   const int C = p.C, W = p.W;
   const int kc = C / BK;                               // channel chunks per tap
-  const int tap0 = split * 9 / splits, ntap = (split + 1) * 9 / splits - tap0;
-  const int KT = ntap * kc;
+  // this split's k-tiles [kt0, kt0 + KT) of the 9 kc (tap, channel chunk) ones
+  const int kt0 = split * 9 * kc / splits, KT = (split + 1) * 9 * kc / splits - kt0;
   const char* act_band = reinterpret_cast<const char*>(p.act_band);
   const char* stale = reinterpret_cast<const char*>(p.stale_act);
   const char* zero = reinterpret_cast<const char*>(p.zero_page);
@@ -217,7 +239,7 @@ __global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p, int
   }
 
   auto issue = [&](int kt, int st) {
-    const int tap = tap0 + kt / kc, c0 = (kt % kc) * BK;
+    const int g = kt0 + kt, tap = g / kc, c0 = (g % kc) * BK;
     const int dy = tap / 3 - 1, dx = tap % 3 - 1;
     char* base = smem + st * STAGE;
 #pragma unroll
@@ -249,7 +271,7 @@ __global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p, int
   // fragment reads: A row 32 wave + (lane & 31), B rows 32 j + (lane & 31),
   // logical chunk 2 kk + (lane >> 5)
   const int frow = lane & 31, h = lane >> 5;
-  const int arow = (32 * wave + frow) * ROWB, brow = BM * ROWB + frow * ROWB;
+  const int arow = (32 * wm + frow) * ROWB, brow = BM * ROWB + (64 * wn + frow) * ROWB;
   int koff[BK / 16];
 #pragma unroll
   for (int kk = 0; kk < BK / 16; ++kk) koff[kk] = ((2 * kk + h) ^ ((frow >> 1) & 7)) * 16;
@@ -272,16 +294,16 @@ __global__ __launch_bounds__(256) void conv3x3_mfma_kernel(UNetConvParams p, int
     }
   }
 
-  // epilogue: lane holds pixel m0 + 32 wave + (lane & 31), channels
-  // n0 + 32 j + 8 g + 4 (lane >> 5) + 0..3 in acc[j][4 g .. 4 g + 3]
-  const int m = m0 + 32 * wave + frow;
+  // epilogue: lane holds pixel m0 + 32 wm + (lane & 31), channels
+  // n0 + 64 wn + 32 j + 8 g + 4 (lane >> 5) + 0..3 in acc[j][4 g .. 4 g + 3]
+  const int m = m0 + 32 * wm + frow;
   if (m >= M) return;
   float* orow = splits > 1 ? p.partial + ((size_t)split * M + m) * p.C_out : p.out + (size_t)m * p.C_out;
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int co = n0 + 32 * j + 8 * g + 4 * h;
+      const int co = n0 + 64 * wn + 32 * j + 8 * g + 4 * h;
       float4 b = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       if (splits == 1) b = *reinterpret_cast<const float4*>(p.bias + co);
       float4 o;
@@ -309,23 +331,53 @@ __global__ __launch_bounds__(256) void conv_split_reduce_kernel(UNetConvParams p
 }
 
 // ---------------------------------------------------------------------------
-// Tap groups of a launch (1, 3 or 9: one per kernel row or per tap): the
-// most whose workgroups stay within a quarter over one round of two per CU,
-// so short bands and deep stages (few pixels, many channels) fill the
-// machine with two workgroups per CU (a lone workgroup per CU runs its
-// k-loop much slower).
-static int conv_splits(int M, int C_out) {
-  const int tiles = ceil_div(M, conv::BM) * (C_out / conv::BN);
-  for (const int s : {9, 3})
-    if (tiles * s <= 2 * 256 * 5 / 4) return s;
-  return 1;
+// K splits of a launch: the 9 C / 64 k-tiles (tap, channel chunk) cut into
+// 1, 3, 9 or 16 even ranges over more workgroups, at least four k-tiles
+// each, the count with the least estimated time.  The estimate (fitted to
+// measurements of the three SDXL-sized stages on MI355X): rounds of
+// workgroups over the slots (256 CUs, two narrow workgroups or one wide per
+// CU) x k-tiles per workgroup x 0.8 us, plus, when split, the fp32
+// partials' round trip at 0.5 us per MB and 3 us for the reduction kernel,
+// which adds them in order.
+static bool conv_wide(int C_out) { return C_out % conv::Wide::BN == 0; }
+
+static int conv_splits(int M, int C, int C_out) {
+  const bool wide = conv_wide(C_out);
+  const int tiles = ceil_div(M, conv::BM) * (C_out / (wide ? conv::Wide::BN : conv::Narrow::BN));
+  const int slots = 256 * (wide ? conv::Wide::WPC : conv::Narrow::WPC);
+  const int kts = 9 * (C / conv::BK);
+  const double mb = (double)M * C_out * sizeof(float) / 1e6;
+  int best = 1;
+  double best_us = 0.0;
+  for (const int s : {1, 3, 9, 16}) {
+    if (s > 1 && kts < 4 * s) break;
+    const double us = ceil_div(tiles * s, slots) * ceil_div(kts, s) * 0.8 + (s > 1 ? s * mb * 0.5 + 3.0 : 0.0);
+    if (s == 1 || us < best_us) {
+      best = s;
+      best_us = us;
+    }
+  }
+  return best;
+}
+
+template <class G>
+static void launch_conv(const UNetConvParams& p, int M, int sp, hipStream_t s) {
+  auto kern = conv3x3_mfma_kernel<G>;
+  static bool attr = [&] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              G::S * G::STAGE);
+    return true;
+  }();
+  (void)attr;
+  const int tiles = ceil_div(M, conv::BM) * (p.C_out / G::BN);
+  hipLaunchKernelGGL(kern, dim3(tiles * sp), dim3(64 * G::NW), G::S * G::STAGE, s, p, sp);
 }
 
 static size_t al256(size_t b) { return (b + 255) / 256 * 256; }
 
 size_t unet_conv_workspace_bytes(int W, int C, int G, int C_out, int rows) {
   const int M = rows * W;
-  const int sp = conv_splits(M, C_out);
+  const int sp = conv_splits(M, C, C_out);
   return al256((size_t)rows * G * 2 * sizeof(float)) + al256((size_t)G * 2 * sizeof(float)) +
          al256((size_t)rows * W * C * sizeof(bf16)) + 256 /* zero page */ +
          (sp > 1 ? al256((size_t)sp * M * C_out * sizeof(float)) : 0);
@@ -335,7 +387,7 @@ hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   UNetConvParams p = p0;
   const int rows = p.row_end - p.row_begin;
   const int M = rows * p.W;
-  const int sp = conv_splits(M, p.C_out);
+  const int sp = conv_splits(M, p.C, p.C_out);
   char* w = reinterpret_cast<char*>(ws);
   p.fresh_sums = reinterpret_cast<float*>(w);
   w += al256((size_t)rows * p.G * 2 * sizeof(float));
@@ -356,14 +408,10 @@ hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   const size_t n4 = (size_t)rows * p.W * p.C / 4;
   const int blocks = (int)std::min<size_t>((n4 + 255) / 256, 4096);
   hipLaunchKernelGGL(gn_silu_kernel, dim3(blocks), dim3(256), 0, s, p);
-  static bool attr = [] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(conv3x3_mfma_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, conv::S * conv::STAGE);
-    return true;
-  }();
-  (void)attr;
-  const int tiles = ceil_div(M, conv::BM) * (p.C_out / conv::BN);
-  hipLaunchKernelGGL(conv3x3_mfma_kernel, dim3(tiles * sp), dim3(256), conv::S * conv::STAGE, s, p, sp);
+  if (conv_wide(p.C_out))
+    launch_conv<conv::Wide>(p, M, sp, s);
+  else
+    launch_conv<conv::Narrow>(p, M, sp, s);
   if (sp > 1) {
     const size_t o4 = (size_t)M * p.C_out / 4;
     hipLaunchKernelGGL(conv_split_reduce_kernel, dim3((int)std::min<size_t>((o4 + 255) / 256, 4096)),

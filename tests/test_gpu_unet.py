@@ -104,14 +104,15 @@ def test_unet_sdxl_deeper_stages(orch_lib, name, rows, share):
     _run(orch_lib, name, rb, re, refresh)
 
 
-def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
+def test_unet_stitching_with_own_buffers(orch_lib):
     """The all-rows pass with refresh fills both buffers; bands then read
-    their halo rows and the other rows' sums from them, and stitch to the
-    all-rows output bit for bit (every output's sum runs in the same order).
-    Bands of 43 rows and more run the convolution unsplit, as the all-rows
-    pass does; shorter ones split the taps over more workgroups (3 groups
-    from 42 rows down, 9 from 14) and add the partial sums in another order,
-    equal up to rounding."""
+    their halo rows and the other rows' sums from them.  Refreshing, the
+    bands rewrite both buffers bit for bit (a row's sums and the group
+    statistics are added in an order fixed by the rows alone), and their
+    outputs stitch to the all-rows output up to the order of the
+    convolution's sums: a launch with few tiles splits its k-tiles over more
+    workgroups and adds their partial sums (the all-rows pass of this stage
+    does not split).  A repeated band gives the same bits."""
     cfg, pr, _, x, _, _ = _setup("unet_sdxl_1024_stage1")
     H, W, C, Co, G = cfg.height, cfg.width, cfg.channels, cfg.out_channels, cfg.groups
     shape = orch_lib.unet_shape(cfg, EPS)
@@ -120,25 +121,31 @@ def test_unet_stitching_with_own_buffers_is_bitwise(orch_lib):
     xd = torch.from_numpy(x).to(DEV)
     act = torch.full((H, W, C), float("nan"), dtype=torch.bfloat16, device=DEV)
     sums = torch.full((H, G, 2), float("nan"), device=DEV)
-    cuts_exact, cuts_split = [0, 56, 128], [0, 16, 40, 72, 73, 128]
-    heights = {H} | {b - a for cuts in (cuts_exact, cuts_split) for a, b in zip(cuts[:-1], cuts[1:])}
+    cut_sets = ([0, 56, 128], [0, 16, 40, 72, 73, 128])
+    heights = {H} | {b - a for cuts in cut_sets for a, b in zip(cuts[:-1], cuts[1:])}
     ws = torch.empty(max(orch_lib.unet_conv_workspace_bytes(shape, r) for r in heights), dtype=torch.uint8,
                      device=DEV)
     full = torch.empty((H, W, Co), device=DEV)
     orch_lib.unet_conv_band(shape, 0, H, xd, dev["gamma"], dev["beta"], wt, dev["bias"], act, sums,
                             1, full, ws)
-    def stitch(cuts):
+    torch.cuda.synchronize()
+    assert not torch.isnan(full).any()
+    act0, sums0 = act.clone(), sums.clone()
+
+    def stitch(cuts, refresh):
         out = torch.empty_like(full)
         for rb, re in zip(cuts[:-1], cuts[1:]):
             o = torch.empty((re - rb, W, Co), device=DEV)
             orch_lib.unet_conv_band(shape, rb, re, xd[rb:re].contiguous(), dev["gamma"], dev["beta"],
-                                    wt, dev["bias"], act, sums, 0, o, ws)
+                                    wt, dev["bias"], act, sums, refresh, o, ws)
             out[rb:re] = o
         torch.cuda.synchronize()
         return out
-    assert not torch.isnan(full).any()
-    assert torch.equal(stitch(cuts_exact), full)
-    assert rel_l2(to_host(stitch(cuts_split)), to_host(full)) <= 1e-6
+    for cuts in cut_sets:
+        got = stitch(cuts, 1)
+        assert torch.equal(act, act0) and torch.equal(sums, sums0), cuts
+        assert rel_l2(to_host(got), to_host(full)) <= 1e-6, cuts
+    assert torch.equal(stitch(cut_sets[1], 0), stitch(cut_sets[1], 0))
 
 
 def test_unet_rejects_bad_arguments(orch_lib):
