@@ -201,7 +201,12 @@ typedef struct {
   float eps;                /* GroupNorm epsilon, > 0                            */
 } orch_unet_conv_shape;
 
-/* Workspace bytes of orch_unet_conv_band for a band of band_rows rows. */
+/* Workspace bytes of orch_unet_conv_band for a band of band_rows rows.  The
+ * need is not monotonic in the height: a call with few convolution tiles
+ * splits its k-tiles over more workgroups and needs room for their fp32
+ * partial sums, so a shorter band can need more than the whole map; a
+ * caller that reuses one workspace sizes it for every height it calls
+ * with. */
 size_t orch_unet_conv_workspace_bytes(const orch_unet_conv_shape* shape, int band_rows);
 
 /* GroupNorm -> SiLU -> conv3x3 on rows [row_begin, row_end) of the map.
