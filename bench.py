@@ -8,17 +8,19 @@ hidden 1152, 16 heads) on a band of token rows of the 64 x 64 token grid
 (fresh K/V for the band, stale buffer for the rest, refreshed in place),
 classifier-free guidance batch 2, and the scheduler update, at the first
 post-warm-up step t 780 -> 760 of the 50-step schedule.  Inputs are seeded
-and synthetic: random N(0, 0.02) weights, N(0, 1) latent, and a seeded
-stale K/V buffer with the spread of the model's K/V (0.02 sqrt(H)).  Every
-hot kernel is launched only at this band's shapes (the per-kernel split times
-the step's own launches), so a profiler's per-kernel averages over the run
-match the figures printed here; --sweep adds the share sweep (other shapes).
+and synthetic: random N(0, 0.02) weights, N(0, 1) latent; the stale K/V
+buffer is what the synchronous warm-up leaves, every token's K/V of a
+full-image step at the previous grid timestep on an independent seeded
+latent, computed by the library before timing.
 
 Prints one JSON line: algorithmic TFLOP/s of the step (value), ms per step,
 the per-kernel split measured inside the steps (HIP events around every
 launch, a second pass after the timed one) with the dominant kernel's
-roofline, optionally the share sweep, and the CPU oracle timed on a bounded
-sample.
+roofline, the HBM-bound kernels at large shapes, the share sweep (10% to
+100% bands; --no-sweep skips it), and the CPU oracle timed on one whole 10%
+band step.  --unet, --schedule and --virtual-devices time the U-Net band
+block, a band's whole sampler schedule and Algorithm 1 over virtual devices
+instead; --pmc-probe / --pmc-report serve the HBM counter runs.
 """
 from __future__ import annotations
 
