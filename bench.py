@@ -38,6 +38,7 @@ PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 METRIC = "patch-step ms and TFLOP/s vs bf16 MFMA peak, DiT-XL/2 1024px, 1 GPU"
 SWEEP_SHARES = (0.10, 0.25, 0.40, 0.65, 1.00)   # elastic band shares of the 1024px grid
+SWEEP_SHARES_2048 = (0.125, 0.375, 0.625)         # band shares of the 2048px grid
 CPU_SHARE = 0.10                                 # band the oracle is timed on, whole step
 PROFILE_ROWS = (4, 8, 16, 32, 64)                # band heights of a device's time profile
 MFMA_KERNELS = ("qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm")
@@ -301,6 +302,42 @@ def step_kernel_split(ctx, cfg, n_q: int, run_step, steps: int):
             rec["bytes_per_launch"] = nbytes[k]
         out[k] = rec
     return out
+
+
+def sweep_2048(torch, L, steps: int) -> dict:
+    """DiT-XL/2 at 2048px (128 token rows, 16384 keys): one band step at each
+    of the 1/8, 3/8 and 5/8 shares at the first stride-2 step of the tiered
+    schedule, the stale buffer filled by a full-image step first (as the
+    1024px bench)."""
+    from paper_2509_04719_amd import schedule as psched
+    from seeded_inputs import configs, generate
+
+    dev = "cuda:0"
+    cfg = configs.get("dit_xl2_2048")
+    t, tp = configs.headline_timestep_pair(cfg)
+    ctx = L.DiTStep(cfg, generate.make_weight_blob(cfg, 0))
+    x = torch.from_numpy(generate.make_latent(cfg, 0)).to(dev)
+    labels = generate.make_labels(cfg, 0)
+    kv = torch.zeros(ctx.stale_kv_bytes() // 2, dtype=torch.bfloat16, device=dev)
+    xs = torch.from_numpy(generate.make_stale_latent(cfg, 0)).to(dev)
+    full_out = torch.empty((cfg.in_ch, cfg.latent, cfg.latent), device=dev)
+    ctx.step(xs, 0, cfg.R, t + cfg.T // cfg.steps, t, labels, cfg.cfg_scale, kv, 1, full_out)
+    del xs, full_out
+    res = {}
+    for share in SWEEP_SHARES_2048:
+        r = psched.band_rows(share, cfg.R)
+        o = torch.empty((cfg.in_ch, r * cfg.patch, cfg.latent), device=dev)
+
+        def band_step():
+            ctx.step(x, 0, r, t, tp, labels, cfg.cfg_scale, kv, 1, o)
+        m = _time_loop(torch, band_step, steps, 2)
+        ks = step_kernel_split(ctx, cfg, cfg.n_q(r), band_step, 2)
+        res[f"{r}/{cfg.R}"] = {"rows": r, "n_q": cfg.n_q(r), "ms": round(m, 3),
+                               "tflops": round(step_flops(cfg, cfg.n_q(r)) / m / 1e9, 1),
+                               "attention_tflops": ks["attention"]["tflops"],
+                               "attention_frac": round(ks["attention"]["tflops"] / PEAK_BF16_TFLOPS, 4)}
+    ctx.close()
+    return {"workload": f"{cfg.name}: {cfg.R} token rows, {cfg.n_kv} keys, t {t}->{tp}", "shares": res}
 
 
 def host_info() -> dict:
@@ -692,7 +729,7 @@ def main(argv=None) -> int:
     hbm = hbm_kernels(torch, L)
     print(f"# HBM-bound kernels at large shapes: {json.dumps(hbm)}", flush=True)
 
-    sweep = {}
+    sweep, sweep2048 = {}, {}
     if not a.no_sweep:
         for share in SWEEP_SHARES:
             r = psched.band_rows(share, cfg.R)
@@ -713,6 +750,8 @@ def main(argv=None) -> int:
                 "attn_gemm_frac": round(ag_fl / ag_ms / 1e9 / PEAK_BF16_TFLOPS, 4),
                 "attention_tflops": ks["attention"]["tflops"]}
         print(f"# sweep: {json.dumps(sweep)}", flush=True)
+        sweep2048 = sweep_2048(torch, L, a.sweep_steps)
+        print(f"# sweep 2048px: {json.dumps(sweep2048)}", flush=True)
 
     cpu = None
     if not a.no_cpu_baseline:
@@ -740,6 +779,7 @@ def main(argv=None) -> int:
         "kernels": split,
         "hbm_kernels": hbm,
         "share_sweep": sweep,
+        "share_sweep_2048": sweep2048,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
