@@ -4,19 +4,20 @@
 // partial sums with the stale partial sums of every other row; the
 // convolution's halo rows come from the stale buffer of its input.
 //
-// Four launches:
+// Three launches (four when the convolution splits its k-tiles):
 //   1. per-row partial sums (sum, sum of squares) of every channel group of
 //      the band's rows (one workgroup per row);
 //   2. the group statistics (mean, 1/sqrt(var + eps)) from every row's sums
-//      (one workgroup, float64 sums);
-//   3. SiLU(GroupNorm(x)) of the band, rounded to bf16, into the buffer's
+//      (float64 sums, taken by every workgroup of this launch), then
+//      SiLU(GroupNorm(x)) of the band, rounded to bf16, into the buffer's
 //      band rows (refresh) or the workspace;
-//   4. the 3x3 convolution as an implicit GEMM on bf16 MFMAs: M = band
+//   3. the 3x3 convolution as an implicit GEMM on bf16 MFMAs: M = band
 //      pixels, N = output channels, K = 9 taps x input channels, fp32
 //      accumulation, bias added in the epilogue.
 // Layouts are pixel-major (NHWC), so a tap's input channels for one pixel are
 // one contiguous run and a 32-channel k-tile of a pixel is 64 bytes.
 #include <algorithm>
+#include <numeric>
 
 #include "common.h"
 #include "kernels.h"
@@ -80,15 +81,15 @@ __global__ __launch_bounds__(kRowSumThreads) void gn_row_sums_kernel(UNetConvPar
   }
 }
 
-// 2. Group statistics over the whole map: band rows from the fresh sums,
+// 2a. Group statistics over the whole map: band rows from the fresh sums,
 // every other row from the stale sums.  256 / G threads per group each add
 // a stride of the rows (independent loads), then the group's shares are
-// added in a fixed order, in float64.
-__global__ __launch_bounds__(256) void gn_stats_kernel(UNetConvParams p) {
+// added in a fixed order, in float64.  Every workgroup of the GroupNorm +
+// SiLU kernel takes them itself into LDS (the same order in each, so the
+// same bits), which spares their own launch.
+__device__ void group_stats(const UNetConvParams& p, float2* stats_lds) {
   __shared__ double red[256][2];
   const int t = threadIdx.x;
-  // the convolution's zero page (read for taps outside the map)
-  if (t < 64) reinterpret_cast<float*>(p.zero_page)[t] = 0.0f;
   const int per = 256 / p.G;                  // G <= 256
   const int g = t % p.G, part = t / p.G;
   const float2* st = reinterpret_cast<const float2*>(p.stale_sums);
@@ -106,44 +107,59 @@ __global__ __launch_bounds__(256) void gn_stats_kernel(UNetConvParams p) {
   red[t][0] = s;
   red[t][1] = q;
   __syncthreads();
-  if (t >= p.G) return;
-  s = 0.0;
-  q = 0.0;
-  for (int k = 0; k < per; ++k) {
-    s += red[k * p.G + t][0];
-    q += red[k * p.G + t][1];
+  if (t < p.G) {
+    s = 0.0;
+    q = 0.0;
+    for (int k = 0; k < per; ++k) {
+      s += red[k * p.G + t][0];
+      q += red[k * p.G + t][1];
+    }
+    const double n = (double)p.H * p.W * (p.C / p.G);
+    const double mean = s / n;
+    const double var = q / n - mean * mean;
+    stats_lds[t] = make_float2((float)mean, (float)(1.0 / sqrt(var + (double)p.eps)));
   }
-  const double n = (double)p.H * p.W * (p.C / p.G);
-  const double mean = s / n;
-  const double var = q / n - mean * mean;
-  reinterpret_cast<float2*>(p.stats)[t] =
-      make_float2((float)mean, (float)(1.0 / sqrt(var + (double)p.eps)));
+  __syncthreads();
 }
 
-// 3. act = SiLU((x - mean) rstd gamma + beta) in bf16, four channels a thread.
+// 2b. act = SiLU((x - mean) rstd gamma + beta) in bf16, four channels a thread
+// (256 threads a workgroup, the statistics first).  The launch's thread count
+// is a multiple of the row's C / 4 channel quads, so a thread keeps one quad
+// for all its elements and folds its statistics and affine into one
+// multiply-add per channel.  Workgroup 0 also clears the convolution's zero
+// page (read for taps outside the map).
+constexpr int kSiluBlocks = 512;
+
 __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
+  __shared__ float2 stats[256];
+  if (blockIdx.x == 0 && threadIdx.x < 64) reinterpret_cast<float*>(p.zero_page)[threadIdx.x] = 0.0f;
+  group_stats(p, stats);
   const size_t n4 = (size_t)(p.row_end - p.row_begin) * p.W * p.C / 4;
+  const size_t first = (size_t)blockIdx.x * 256 + threadIdx.x, stride = (size_t)gridDim.x * 256;
   const int Q = p.C / 4, cg = p.C / p.G;
-  const float2* stats = reinterpret_cast<const float2*>(p.stats);
-  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) {
-    const int c0 = (int)(i % Q) * 4;
+  const int c0 = (int)(first % Q) * 4;
+  const float4 gm = reinterpret_cast<const float4*>(p.gamma)[c0 / 4];
+  const float4 bt = reinterpret_cast<const float4*>(p.beta)[c0 / 4];
+  const float gv[4] = {gm.x, gm.y, gm.z, gm.w}, bv[4] = {bt.x, bt.y, bt.z, bt.w};
+  float mul[4], add[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float2 sr = stats[(c0 + k) / cg];
+    mul[k] = sr.y * gv[k];
+    add[k] = bv[k] - sr.x * mul[k];
+  }
+  for (size_t i = first; i < n4; i += stride) {
     const float4 v = reinterpret_cast<const float4*>(p.x)[i];
-    const float4 gm = reinterpret_cast<const float4*>(p.gamma)[c0 / 4];
-    const float4 bt = reinterpret_cast<const float4*>(p.beta)[c0 / 4];
-    const float xv[4] = {v.x, v.y, v.z, v.w}, gv[4] = {gm.x, gm.y, gm.z, gm.w},
-                bv[4] = {bt.x, bt.y, bt.z, bt.w};
+    const float xv[4] = {v.x, v.y, v.z, v.w};
     bf16x4 o;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float2 sr = stats[(c0 + k) / cg];
-      o[k] = (bf16)silu_f((xv[k] - sr.x) * sr.y * gv[k] + bv[k]);
-    }
+    for (int k = 0; k < 4; ++k) o[k] = (bf16)silu_f(fmaf(xv[k], mul[k], add[k]));
     reinterpret_cast<bf16x4*>(p.act_band)[i] = o;
   }
 }
 
 // ---------------------------------------------------------------------------
-// 4. The convolution as an implicit GEMM.  Workgroup tile: 128 band pixels x
+// 3. The convolution as an implicit GEMM.  Workgroup tile: 128 band pixels x
 // 64 output channels, four waves of 32 pixels (or x 128 channels, eight
 // waves, see below); k-tiles of one tap x 64 input channels (128-byte rows),
 // loaded straight into LDS (16 bytes per lane, no register staging) into a
@@ -378,7 +394,7 @@ static size_t al256(size_t b) { return (b + 255) / 256 * 256; }
 size_t unet_conv_workspace_bytes(int W, int C, int G, int C_out, int rows) {
   const int M = rows * W;
   const int sp = conv_splits(M, C, C_out);
-  return al256((size_t)rows * G * 2 * sizeof(float)) + al256((size_t)G * 2 * sizeof(float)) +
+  return al256((size_t)rows * G * 2 * sizeof(float)) +
          al256((size_t)rows * W * C * sizeof(bf16)) + 256 /* zero page */ +
          (sp > 1 ? al256((size_t)sp * M * C_out * sizeof(float)) : 0);
 }
@@ -391,8 +407,6 @@ hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   char* w = reinterpret_cast<char*>(ws);
   p.fresh_sums = reinterpret_cast<float*>(w);
   w += al256((size_t)rows * p.G * 2 * sizeof(float));
-  p.stats = reinterpret_cast<float*>(w);
-  w += al256((size_t)p.G * 2 * sizeof(float));
   void* act_ws = w;
   w += al256((size_t)rows * p.W * p.C * sizeof(bf16));
   p.zero_page = w;
@@ -404,9 +418,12 @@ hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   const int q4 = p.C / 4, shares = q4 <= kRowSumThreads ? kRowSumThreads / q4 : 1;
   hipLaunchKernelGGL(gn_row_sums_kernel, dim3(rows), dim3(kRowSumThreads),
                      (size_t)shares * 2 * p.C * sizeof(float), s, p);
-  hipLaunchKernelGGL(gn_stats_kernel, dim3(1), dim3(256), 0, s, p);
+  // workgroups: enough for the band (at most kSiluBlocks), a multiple of
+  // Q / gcd(Q, 256) so that 256 * blocks is a multiple of the C / 4 quads
   const size_t n4 = (size_t)rows * p.W * p.C / 4;
-  const int blocks = (int)std::min<size_t>((n4 + 255) / 256, 4096);
+  const int nq = p.C / 4, unit = nq / std::gcd(nq, 256);
+  int blocks = (int)std::min<size_t>((n4 + 255) / 256, kSiluBlocks);
+  blocks = std::max(unit, blocks / unit * unit);
   hipLaunchKernelGGL(gn_silu_kernel, dim3(blocks), dim3(256), 0, s, p);
   if (conv_wide(p.C_out))
     launch_conv<conv::Wide>(p, M, sp, s);

@@ -145,7 +145,6 @@ struct UNetConvParams {
   float eps;
   // set by the launcher: workspace parts, and where the band's activations go
   float* fresh_sums;          // fp32 [rows][G][2]
-  float* stats;               // fp32 [G][2]: mean, 1/sqrt(var + eps)
   void* act_band;             // bf16 [rows][W][C]
   void* zero_page;            // 256 zero bytes (taps outside the map)
   float* partial;             // split launch: fp32 [splits][rows * W][C_out]
