@@ -9,13 +9,15 @@
 //      the band's rows (one workgroup per row);
 //   2. the group statistics (mean, 1/sqrt(var + eps)) from every row's sums
 //      (float64 sums, taken by every workgroup of this launch), then
-//      SiLU(GroupNorm(x)) of the band, rounded to bf16, into the buffer's
-//      band rows (refresh) or the workspace;
-//   3. the 3x3 convolution as an implicit GEMM on bf16 MFMAs: M = band
-//      pixels, N = output channels, K = 9 taps x input channels, fp32
-//      accumulation, bias added in the epilogue.
+//      SiLU(GroupNorm(x)) of the band, rounded to bf16, into a zero-bordered
+//      tile of the band (one more row above and below, from the stale buffer
+//      or zero outside the map, and a zero column on each side) and, on a
+//      refresh, into the buffer's band rows;
+//   3. the 3x3 convolution as an implicit GEMM on bf16 MFMAs over the tile:
+//      M = band pixels, N = output channels, K = 9 taps x input channels,
+//      fp32 accumulation, bias added in the epilogue.
 // Layouts are pixel-major (NHWC), so a tap's input channels for one pixel are
-// one contiguous run and a 32-channel k-tile of a pixel is 64 bytes.
+// one contiguous run and a 64-channel k-tile of a pixel is 128 bytes.
 #include <algorithm>
 #include <numeric>
 
@@ -126,17 +128,20 @@ __device__ void group_stats(const UNetConvParams& p, float2* stats_lds) {
 // (256 threads a workgroup, the statistics first).  The launch's thread count
 // is a multiple of the row's C / 4 channel quads, so a thread keeps one quad
 // for all its elements and folds its statistics and affine into one
-// multiply-add per channel.  Workgroup 0 also clears the convolution's zero
-// page (read for taps outside the map).
+// multiply-add per channel.  The result goes to the interior of the padded
+// tile [rows + 2][W + 2][C] (pixel (y, x) of the band at tile row y + 1,
+// column x + 1) and, on a refresh, to the band rows of the stale buffer.  The
+// tile's border follows: its first and last rows are the stale rows above
+// and below the band (zero outside the map), its first and last columns zero.
 constexpr int kSiluBlocks = 512;
 
 __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
   __shared__ float2 stats[256];
-  if (blockIdx.x == 0 && threadIdx.x < 64) reinterpret_cast<float*>(p.zero_page)[threadIdx.x] = 0.0f;
   group_stats(p, stats);
-  const size_t n4 = (size_t)(p.row_end - p.row_begin) * p.W * p.C / 4;
-  const size_t first = (size_t)blockIdx.x * 256 + threadIdx.x, stride = (size_t)gridDim.x * 256;
-  const int Q = p.C / 4, cg = p.C / p.G;
+  const int rows = p.row_end - p.row_begin, W = p.W, Q = p.C / 4, cg = p.C / p.G;
+  // every index below fits 32 bits: the launcher keeps the tile under 2^31 bytes
+  const unsigned n4 = (unsigned)rows * W * Q;
+  const unsigned first = blockIdx.x * 256u + threadIdx.x, stride = gridDim.x * 256u;
   const int c0 = (int)(first % Q) * 4;
   const float4 gm = reinterpret_cast<const float4*>(p.gamma)[c0 / 4];
   const float4 bt = reinterpret_cast<const float4*>(p.beta)[c0 / 4];
@@ -148,29 +153,65 @@ __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
     mul[k] = sr.y * gv[k];
     add[k] = bv[k] - sr.x * mul[k];
   }
-  for (size_t i = first; i < n4; i += stride) {
+  bf16x4* tile = reinterpret_cast<bf16x4*>(p.act_pad);
+  bf16x4* band = p.refresh ? reinterpret_cast<bf16x4*>(p.stale_act) + (size_t)p.row_begin * W * Q : nullptr;
+  const float inv_w = 1.0f / (float)W;
+  for (unsigned i = first; i < n4; i += stride) {
     const float4 v = reinterpret_cast<const float4*>(p.x)[i];
     const float xv[4] = {v.x, v.y, v.z, v.w};
     bf16x4 o;
 #pragma unroll
     for (int k = 0; k < 4; ++k) o[k] = (bf16)silu_f(fmaf(xv[k], mul[k], add[k]));
-    reinterpret_cast<bf16x4*>(p.act_band)[i] = o;
+    // band pixel px = (y, x) -> tile pixel (y + 1) (W + 2) + x + 1 = px + 2 y + W + 3
+    const int px = (int)(i / Q);
+    int y = (int)(((float)px + 0.5f) * inv_w);
+    y -= y * W > px;
+    y += (y + 1) * W <= px;
+    tile[(unsigned)(px + 2 * y + W + 3) * Q + (i - (unsigned)px * Q)] = o;
+    if (band) band[i] = o;
+  }
+  // border: 2 (W + 2) Q quads of the halo rows, then 2 rows Q of the side columns
+  const unsigned halo = 2u * (W + 2) * Q, nb = halo + 2u * rows * Q;
+  const bf16x4* stale = reinterpret_cast<const bf16x4*>(p.stale_act);
+  for (unsigned i = first; i < nb; i += stride) {
+    bf16x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = (bf16)0.0f;
+    unsigned dst;
+    if (i < halo) {
+      const unsigned below = i / ((W + 2) * Q);
+      const unsigned r = i - below * (W + 2) * Q;
+      const int col = (int)(r / Q), q = (int)(r % Q);
+      const int sy = below ? p.row_end : p.row_begin - 1;
+      if (col >= 1 && col <= W && sy >= 0 && sy < p.H) o = stale[((size_t)sy * W + col - 1) * Q + q];
+      dst = ((below ? rows + 1 : 0) * (W + 2) + col) * Q + q;
+    } else {
+      const unsigned r = i - halo;
+      const int y = (int)(r / (2 * Q)), side = (int)(r / Q) & 1, q = (int)(r % Q);
+      dst = ((unsigned)(y + 1) * (W + 2) + (side ? W + 1 : 0)) * Q + q;
+    }
+    tile[dst] = o;
   }
 }
 
 // ---------------------------------------------------------------------------
-// 3. The convolution as an implicit GEMM.  Workgroup tile: 128 band pixels x
-// 64 output channels, four waves of 32 pixels (or x 128 channels, eight
-// waves, see below); k-tiles of one tap x 64 input channels (128-byte rows),
-// loaded straight into LDS (16 bytes per lane, no register staging) into a
-// ring of stages, one barrier per k-tile.  A
-// lane of a wave-level load fills LDS row (lane / 8) of its 8-row slab at
-// physical chunk lane % 8, holding logical chunk (lane % 8) ^ ((row / 2) % 8):
-// the fragment reads (16 rows at one logical chunk) then hit distinct banks.
-// The A rows are gathered per tap: the pixel shifted by (dy - 1, dx - 1),
-// read from the band's activations, the stale buffer (halo rows) or a zero
-// page (outside the map).  The MFMAs take the weight rows as the first
-// operand, so a lane ends with four consecutive output channels of one pixel.
+// 3. The convolution as an implicit GEMM over the padded tile.  Workgroup
+// tile: 128 band pixels x 64 output channels on four waves (or x 128 channels
+// on eight, see below), each wave 32 pixels x 64 channels; k-tiles of one tap
+// x 64 input channels (128-byte rows), loaded straight into LDS (16 bytes per
+// lane, no register staging) into a ring of stages, one barrier per k-tile.
+// In the padded tile the tap (dy, dx) of every pixel is the pixel's own
+// address plus one uniform offset, so a lane's source is a constant per-lane
+// offset plus a scalar per k-tile, for the weights as for the activations,
+// and a load costs no vector arithmetic.  A lane of a wave-level load fills
+// LDS row (lane / 8) of its 8-row slab at physical chunk lane % 8, holding
+// logical chunk (lane % 8) ^ ((row / 2) % 8): the fragment reads (16 rows at
+// one logical chunk) then hit distinct banks.  The MFMAs take the weight rows
+// as the first operand, so a lane ends with four consecutive output channels
+// of one pixel.  The main loop's emission order is fixed with scheduling
+// fences: each MFMA, then its share of the next k-step's fragment reads, then
+// its share of the next tile's loads.  The epilogue stages each wave's 32 x 64
+// block in LDS and writes whole 256-byte runs of a pixel's channels.
 // Launches with few tiles split their k-tiles (tap, channel chunk) in even
 // ranges over more workgroups; the fp32 partial sums are added in order by a
 // second kernel, which adds the bias.  Output widths divisible by 128 take
@@ -178,6 +219,8 @@ __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
 namespace conv {
 constexpr int BM = 128, BK = 64;
 constexpr int ROWB = 2 * BK;                         // bytes per LDS row
+constexpr int KK = BK / 16;                          // MFMA k-steps per k-tile
+constexpr int SROW = 64 + 4;                         // epilogue strip row (floats)
 // BN output channels per workgroup over NW waves (each 32 pixels x 64
 // channels), a ring of S stages
 template <int BN_, int NW_, int S_>
@@ -187,10 +230,12 @@ struct Geo {
   static constexpr int LA = BM * ROWB / (NW * 1024);  // A loads per lane per k-tile
   static constexpr int LB = BN * ROWB / (NW * 1024);  // B loads per lane per k-tile
   static constexpr int LPT = LA + LB;
+  static constexpr int LPK = (LPT + KK - 1) / KK;     // loads issued per k-step
   static constexpr int WPC = 160 * 1024 / (S * STAGE);  // workgroups per CU (LDS)
   static_assert(NW * 64 == 4 * BN, "four waves of 32 pixels per 64 channels");
   static_assert(LA * NW * 1024 == BM * ROWB && LB * NW * 1024 == BN * ROWB, "whole wave-level loads");
   static_assert(S >= 2 && S <= 4 && (S - 1) * LPT < 64, "ring depth");
+  static_assert(NW * 32 * SROW * 4 <= S * STAGE, "epilogue strips fit the ring");
 };
 // 64 channels: 24 KB stages, three, two workgroups of four waves per CU;
 // 128 channels (output widths divisible by 128): 32 KB stages, four, one
@@ -199,18 +244,10 @@ using Narrow = Geo<64, 4, 3>;
 using Wide = Geo<128, 8, 4>;
 }
 
-template <int LPTn>
-__device__ __forceinline__ void conv_wait(int tiles_after) {
-  if (tiles_after >= 3) wait_vmcnt<3 * LPTn>();
-  else if (tiles_after == 2) wait_vmcnt<2 * LPTn>();
-  else if (tiles_after == 1) wait_vmcnt<LPTn>();
-  else wait_vmcnt<0>();
-}
-
 template <class G>
 __global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams p, int splits) {
   using namespace conv;
-  constexpr int BN = G::BN, NW = G::NW, S = G::S, STAGE = G::STAGE, LA = G::LA, LB = G::LB, LPT = G::LPT;
+  constexpr int NW = G::NW, S = G::S, STAGE = G::STAGE, LA = G::LA, LPT = G::LPT, LPK = G::LPK;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -218,64 +255,48 @@ __global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams
   const int wm = wave % 4, wn = wave / 4;
   const int rows = p.row_end - p.row_begin;
   const int M = rows * p.W;
-  const int tiles_n = p.C_out / BN;
+  const int tiles_n = p.C_out / G::BN;
   const int tiles = ceil_div(M, BM) * tiles_n;
   const int split = __builtin_amdgcn_readfirstlane((int)blockIdx.x / tiles);
   const int tile = blockIdx.x - split * tiles;
-  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
-  const int C = p.C, W = p.W;
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * G::BN;
+  const int C = p.C, W = p.W, WP = p.W + 2;
   const int kc = C / BK;                               // channel chunks per tap
   // this split's k-tiles [kt0, kt0 + KT) of the 9 kc (tap, channel chunk) ones
   const int kt0 = split * 9 * kc / splits, KT = (split + 1) * 9 * kc / splits - kt0;
-  const char* act_band = reinterpret_cast<const char*>(p.act_band);
-  const char* stale = reinterpret_cast<const char*>(p.stale_act);
-  const char* zero = reinterpret_cast<const char*>(p.zero_page);
-  const char* wgt = reinterpret_cast<const char*>(p.weight);
+  const char* gA = reinterpret_cast<const char*>(p.act_pad);
+  const char* gW = reinterpret_cast<const char*>(p.weight);
 
-  // this lane's load slots: A rows 8 (i NW + wave) + lane / 8 (pixel of the
-  // tile), B rows likewise (output channel); logical chunk of the slot
+  // this lane's sources: load j covers slab rows 8 (i NW + wave) + lane / 8
+  // of the A rows (pixels; rows past M re-read pixel M - 1), then of the B
+  // rows (output channels), at logical chunk (lane % 8) ^ ((row / 2) % 8);
+  // byte offsets of tap (0, 0), channel chunk 0
   const int lrow = lane >> 3, pc = lane & 7;
-  int ay[LA], ax[LA], alc[LA];
-  bool aon[LA];
+  unsigned off[LPT];
 #pragma unroll
-  for (int i = 0; i < LA; ++i) {
+  for (int j = 0; j < LPT; ++j) {
+    const int i = j < LA ? j : j - LA;
     const int r = 8 * (i * NW + wave) + lrow;
-    const int m = m0 + r;
-    aon[i] = m < M;
-    const int mm = aon[i] ? m : 0;
-    ay[i] = p.row_begin + mm / W;
-    ax[i] = mm % W;
-    alc[i] = pc ^ ((r >> 1) & 7);
-  }
-  size_t boff[LB];
-#pragma unroll
-  for (int i = 0; i < LB; ++i) {
-    const int r = 8 * (i * NW + wave) + lrow;
-    boff[i] = ((size_t)(n0 + r) * 9 * C + (size_t)(pc ^ ((r >> 1) & 7)) * 8) * 2;
-  }
-
-  auto issue = [&](int kt, int st) {
-    const int g = kt0 + kt, tap = g / kc, c0 = (g % kc) * BK;
-    const int dy = tap / 3 - 1, dx = tap % 3 - 1;
-    char* base = smem + st * STAGE;
-#pragma unroll
-    for (int i = 0; i < LA; ++i) {
-      const int sy = ay[i] + dy, sx = ax[i] + dx;
-      const char* src = zero;
-      if (aon[i] && sx >= 0 && sx < W && sy >= 0 && sy < p.H) {
-        src = (sy >= p.row_begin && sy < p.row_end)
-                  ? act_band + (((size_t)(sy - p.row_begin) * W + sx) * C + c0 + alc[i] * 8) * 2
-                  : stale + (((size_t)sy * W + sx) * C + c0 + alc[i] * 8) * 2;
-      }
-      __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src,
-                                       (ORCH_LDS void*)(base + (i * NW + wave) * 1024), 16, 0, 0);
+    const unsigned lc = (unsigned)(pc ^ ((r >> 1) & 7)) * 16u;
+    if (j < LA) {
+      const int m = min(m0 + r, M - 1), y = m / W;
+      off[j] = (unsigned)((y + 1) * WP + (m - y * W) + 1) * (unsigned)C * 2u + lc;
+    } else {
+      off[j] = (unsigned)(n0 + r) * (unsigned)(9 * C) * 2u + lc;
     }
-#pragma unroll
-    for (int i = 0; i < LB; ++i) {
-      const char* src = wgt + boff[i] + ((size_t)tap * C + c0) * 2;
-      __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src,
-                                       (ORCH_LDS void*)(base + BM * ROWB + (i * NW + wave) * 1024), 16, 0, 0);
-    }
+  }
+  // scalar offsets of k-tile g: the tap's shift in the padded tile plus the
+  // channel chunk (A); g 128-byte k-tiles into each weight row (B)
+  auto a_shift = [&](int g) -> int {
+    const int tap = g / kc, dy = tap / 3 - 1, dx = tap % 3 - 1;
+    return ((dy * WP + dx) * C + (g - tap * kc) * BK) * 2;
+  };
+  auto dma = [&](auto jc, int g, int ashift, int st) {
+    constexpr int j = decltype(jc)::value;
+    constexpr int i = j < LA ? j : j - LA;
+    char* dst = smem + st * STAGE + (j < LA ? 0 : BM * ROWB) + (i * NW + wave) * 1024;
+    const char* src = j < LA ? gA + ashift + off[j] : gW + g * ROWB + off[j];
+    __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src, (ORCH_LDS void*)dst, 16, 0, 0);
   };
 
   f32x16 acc[2];
@@ -284,51 +305,96 @@ __global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
 
-  // fragment reads: A row 32 wave + (lane & 31), B rows 32 j + (lane & 31),
+  // fragment reads: A row 32 wm + (lane & 31), B rows 64 wn + 32 j + (lane & 31),
   // logical chunk 2 kk + (lane >> 5)
   const int frow = lane & 31, h = lane >> 5;
   const int arow = (32 * wm + frow) * ROWB, brow = BM * ROWB + (64 * wn + frow) * ROWB;
-  int koff[BK / 16];
+  int koff[KK];
 #pragma unroll
-  for (int kk = 0; kk < BK / 16; ++kk) koff[kk] = ((2 * kk + h) ^ ((frow >> 1) & 7)) * 16;
+  for (int kk = 0; kk < KK; ++kk) koff[kk] = ((2 * kk + h) ^ ((frow >> 1) & 7)) * 16;
 
-  const int pro = min(S - 1, KT);
-  for (int t = 0; t < pro; ++t) issue(t, t);
-  for (int kt = 0; kt < KT; ++kt) {
-    conv_wait<LPT>(min(KT, kt + S - 1) - (kt + 1));
-    lds_barrier();
-    if (kt + S - 1 < KT) issue(kt + S - 1, (kt + S - 1) % S);
-    const char* base = smem + (kt % S) * STAGE;
+  // the MFMAs of stage st; with ISSUE, k-tile ig's loads into stage ist go
+  // between them: MFMA e of k-step kk, its share of k-step kk + 1's three
+  // fragment reads, its share of the loads
+  auto compute = [&](int st, auto issue_c, int ig, int ist) {
+    constexpr bool ISSUE = decltype(issue_c)::value;
+    const char* base = smem + st * STAGE;
+    const int ash = ISSUE ? a_shift(ig) : 0;
+    bf16x8 fa[2], fb[2][2];
+    fa[0] = *reinterpret_cast<const bf16x8*>(base + arow + koff[0]);
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const bf16x8 fa = *reinterpret_cast<const bf16x8*>(base + arow + koff[kk]);
+    for (int j = 0; j < 2; ++j) fb[0][j] = *reinterpret_cast<const bf16x8*>(base + brow + j * 32 * ROWB + koff[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, KK>([&](auto kkc) {
+      constexpr int kk = decltype(kkc)::value;
+      constexpr int cur = kk & 1;
+      constexpr int nd = kk + 1 < KK ? 3 : 0;
+      constexpr int l0 = cmin(kk * LPK, LPT), nl = ISSUE ? cmin(kk * LPK + LPK, LPT) - l0 : 0;
+      static_for<0, 2>([&](auto ec) {
+        constexpr int e = decltype(ec)::value;
+        acc[e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][e], fa[cur], acc[e], 0, 0, 0);
+        static_for<e * nd / 2, (e + 1) * nd / 2>([&](auto dc) {
+          constexpr int d = decltype(dc)::value;
+          if constexpr (d == 0)
+            fa[cur ^ 1] = *reinterpret_cast<const bf16x8*>(base + arow + koff[cmin(kk + 1, KK - 1)]);
+          else
+            fb[cur ^ 1][d - 1] = *reinterpret_cast<const bf16x8*>(base + brow + (d - 1) * 32 * ROWB +
+                                                                   koff[cmin(kk + 1, KK - 1)]);
+        });
+        static_for<l0 + e * nl / 2, l0 + (e + 1) * nl / 2>([&](auto jc) { dma(jc, ig, ash, ist); });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
+  };
+
+  // prologue: k-tiles 0 .. S - 2 (KT >= S - 1: at least four k-tiles a split)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const bf16x8 fw = *reinterpret_cast<const bf16x8*>(base + brow + j * 32 * ROWB + koff[kk]);
-        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw, fa, acc[j], 0, 0, 0);
-      }
-    }
+  for (int t = 0; t < S - 1; ++t) {
+    const int ash = a_shift(kt0 + t);
+    static_for<0, LPT>([&](auto jc) { dma(jc, kt0 + t, ash, t); });
   }
+  int kt = 0;
+  for (; kt + S - 1 < KT; ++kt) {
+    wait_vmcnt<(S - 2) * LPT>();
+    lds_barrier();
+    compute(kt % S, std::true_type{}, kt0 + kt + S - 1, (kt + S - 1) % S);
+  }
+  // drain: the last S - 1 k-tiles, nothing more to issue
+  static_for<0, S - 2>([&](auto rc) {
+    wait_vmcnt<(S - 2 - decltype(rc)::value) * LPT>();
+    lds_barrier();
+    compute(kt % S, std::false_type{}, 0, 0);
+    ++kt;
+  });
+  wait_vmcnt<0>();
+  lds_barrier();
+  compute(kt % S, std::false_type{}, 0, 0);
 
-  // epilogue: lane holds pixel m0 + 32 wm + (lane & 31), channels
-  // n0 + 64 wn + 32 j + 8 g + 4 (lane >> 5) + 0..3 in acc[j][4 g .. 4 g + 3]
-  const int m = m0 + 32 * wm + frow;
-  if (m >= M) return;
-  float* orow = splits > 1 ? p.partial + ((size_t)split * M + m) * p.C_out : p.out + (size_t)m * p.C_out;
+  // epilogue: lane holds pixel 32 wm + (lane & 31), channels 64 wn + 32 j +
+  // 8 g + 4 (lane >> 5) + 0..3 in acc[j][4 g .. 4 g + 3]; through a per-wave
+  // strip in LDS, each pixel's 64 channels leave as 16 lanes x 16 bytes
+  lds_barrier();
+  float* strip = reinterpret_cast<float*>(smem) + wave * 32 * SROW;
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int co = n0 + 64 * wn + 32 * j + 8 * g + 4 * h;
-      float4 b = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      if (splits == 1) b = *reinterpret_cast<const float4*>(p.bias + co);
-      float4 o;
-      o.x = acc[j][4 * g + 0] + b.x;
-      o.y = acc[j][4 * g + 1] + b.y;
-      o.z = acc[j][4 * g + 2] + b.z;
-      o.w = acc[j][4 * g + 3] + b.w;
-      *reinterpret_cast<float4*>(orow + co) = o;
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4*>(strip + frow * SROW + 32 * j + 8 * g + 4 * h) =
+          make_float4(acc[j][4 * g], acc[j][4 * g + 1], acc[j][4 * g + 2], acc[j][4 * g + 3]);
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the strip is written
+  const int q = lane & 15, co = n0 + 64 * wn + 4 * q;
+  float4 b = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (splits == 1) b = *reinterpret_cast<const float4*>(p.bias + co);
+  float* obase = splits > 1 ? p.partial + (size_t)split * M * p.C_out : p.out;
+#pragma unroll
+  for (int r0 = 0; r0 < 32; r0 += 4) {
+    const int r = r0 + (lane >> 4), m = m0 + 32 * wm + r;
+    if (m < M) {
+      const float4 v = *reinterpret_cast<const float4*>(strip + r * SROW + 4 * q);
+      *reinterpret_cast<float4*>(obase + (size_t)m * p.C_out + co) =
+          make_float4(v.x + b.x, v.y + b.y, v.z + b.z, v.w + b.w);
     }
+  }
 }
 
 // The split launch's partial sums, added in split order, plus the bias.
@@ -349,12 +415,12 @@ __global__ __launch_bounds__(256) void conv_split_reduce_kernel(UNetConvParams p
 // ---------------------------------------------------------------------------
 // K splits of a launch: the 9 C / 64 k-tiles (tap, channel chunk) cut into
 // 1, 3, 9 or 16 even ranges over more workgroups, at least four k-tiles
-// each, the count with the least estimated time.  The estimate (fitted to
-// measurements of the three SDXL-sized stages on MI355X): rounds of
-// workgroups over the slots (256 CUs, two narrow workgroups or one wide per
-// CU) x k-tiles per workgroup x 0.8 us, plus, when split, the fp32
-// partials' round trip at 0.5 us per MB and 3 us for the reduction kernel,
-// which adds them in order.
+// each, the count with the least estimated time.  The estimate (fitted by
+// least squares to every split count of twelve bands of the three SDXL-sized
+// stages on MI355X, 2 us rms): rounds of workgroups over the slots (256 CUs,
+// two narrow workgroups or one wide per CU) x k-tiles per workgroup x 0.36
+// us, plus, when split, the fp32 partials' round trip (written by the
+// convolution, added in order by the reduction kernel) at 0.43 us per MB.
 static bool conv_wide(int C_out) { return C_out % conv::Wide::BN == 0; }
 
 static int conv_splits(int M, int C, int C_out) {
@@ -367,7 +433,7 @@ static int conv_splits(int M, int C, int C_out) {
   double best_us = 0.0;
   for (const int s : {1, 3, 9, 16}) {
     if (s > 1 && kts < 4 * s) break;
-    const double us = ceil_div(tiles * s, slots) * ceil_div(kts, s) * 0.8 + (s > 1 ? s * mb * 0.5 + 3.0 : 0.0);
+    const double us = ceil_div(tiles * s, slots) * ceil_div(kts, s) * 0.36 + (s > 1 ? s * mb * 0.43 : 0.0);
     if (s == 1 || us < best_us) {
       best = s;
       best_us = us;
@@ -395,7 +461,7 @@ size_t unet_conv_workspace_bytes(int W, int C, int G, int C_out, int rows) {
   const int M = rows * W;
   const int sp = conv_splits(M, C, C_out);
   return al256((size_t)rows * G * 2 * sizeof(float)) +
-         al256((size_t)rows * W * C * sizeof(bf16)) + 256 /* zero page */ +
+         al256((size_t)(rows + 2) * (W + 2) * C * sizeof(bf16)) +
          (sp > 1 ? al256((size_t)sp * M * C_out * sizeof(float)) : 0);
 }
 
@@ -407,14 +473,9 @@ hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   char* w = reinterpret_cast<char*>(ws);
   p.fresh_sums = reinterpret_cast<float*>(w);
   w += al256((size_t)rows * p.G * 2 * sizeof(float));
-  void* act_ws = w;
-  w += al256((size_t)rows * p.W * p.C * sizeof(bf16));
-  p.zero_page = w;
-  w += 256;
+  p.act_pad = w;
+  w += al256((size_t)(rows + 2) * (p.W + 2) * p.C * sizeof(bf16));
   p.partial = sp > 1 ? reinterpret_cast<float*>(w) : nullptr;
-  // the band's activations: straight into the buffer's band rows on a refresh
-  p.act_band = p.refresh ? reinterpret_cast<char*>(p.stale_act) + (size_t)p.row_begin * p.W * p.C * sizeof(bf16)
-                         : act_ws;
   const int q4 = p.C / 4, shares = q4 <= kRowSumThreads ? kRowSumThreads / q4 : 1;
   hipLaunchKernelGGL(gn_row_sums_kernel, dim3(rows), dim3(kRowSumThreads),
                      (size_t)shares * 2 * p.C * sizeof(float), s, p);

@@ -145,11 +145,13 @@ struct UNetConvParams {
   float eps;
   // set by the launcher: workspace parts, and where the band's activations go
   float* fresh_sums;          // fp32 [rows][G][2]
-  void* act_band;             // bf16 [rows][W][C]
-  void* zero_page;            // 256 zero bytes (taps outside the map)
+  void* act_pad;              // bf16 [rows + 2][W + 2][C]: the band's activations, zero-bordered,
+                              // with the stale rows above and below
   float* partial;             // split launch: fp32 [splits][rows * W][C_out]
 };
 size_t unet_conv_workspace_bytes(int W, int C, int G, int C_out, int rows);
+// Largest padded activation tile (bytes) the kernels index with 32-bit offsets.
+constexpr size_t kUNetMaxTileBytes = (size_t)1 << 31;
 hipError_t launch_unet_conv(const UNetConvParams& p, void* workspace, hipStream_t stream);
 
 }  // namespace orch

@@ -985,6 +985,9 @@ int check_unet_shape(const orch_unet_conv_shape* s) {
     return fail(ORCH_EINVAL, "groups must divide channels and be <= 256");
   if (s->out_channels < 64 || s->out_channels % 64) return fail(ORCH_EINVAL, "out_channels must be a positive multiple of 64");
   if (!(s->eps > 0.0f) || !std::isfinite(s->eps)) return fail(ORCH_EINVAL, "eps must be finite and > 0");
+  if ((size_t)(s->height + 2) * (s->width + 2) * s->channels * 2 >= kUNetMaxTileBytes ||
+      (size_t)s->out_channels * 9 * s->channels * 2 >= kUNetMaxTileBytes)
+    return fail(ORCH_EINVAL, "map or weight too large (2 GiB or more in bf16)");
   return ORCH_OK;
 }
 }  // namespace
