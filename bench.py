@@ -604,7 +604,7 @@ def unet_cpu_baseline(cfg, rb, re):
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="dit_xl2_1024")
     ap.add_argument("--share", type=float, default=0.40)

@@ -20,6 +20,7 @@
 // one contiguous run and a 64-channel k-tile of a pixel is 128 bytes.
 #include <algorithm>
 #include <numeric>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -196,63 +197,73 @@ __global__ __launch_bounds__(256) void gn_silu_kernel(UNetConvParams p) {
 
 // ---------------------------------------------------------------------------
 // 3. The convolution as an implicit GEMM over the padded tile.  Workgroup
-// tile: 128 band pixels x 64 output channels on four waves (or x 128 channels
-// on eight, see below), each wave 32 pixels x 64 channels; k-tiles of one tap
-// x 64 input channels (128-byte rows), loaded straight into LDS (16 bytes per
-// lane, no register staging) into a ring of stages, one barrier per k-tile.
-// In the padded tile the tap (dy, dx) of every pixel is the pixel's own
-// address plus one uniform offset, so a lane's source is a constant per-lane
-// offset plus a scalar per k-tile, for the weights as for the activations,
-// and a load costs no vector arithmetic.  A lane of a wave-level load fills
-// LDS row (lane / 8) of its 8-row slab at physical chunk lane % 8, holding
-// logical chunk (lane % 8) ^ ((row / 2) % 8): the fragment reads (16 rows at
-// one logical chunk) then hit distinct banks.  The MFMAs take the weight rows
-// as the first operand, so a lane ends with four consecutive output channels
-// of one pixel.  The main loop's emission order is fixed with scheduling
-// fences: each MFMA, then its share of the next k-step's fragment reads, then
-// its share of the next tile's loads.  The epilogue stages each wave's 32 x 64
-// block in LDS and writes whole 256-byte runs of a pixel's channels.
-// Launches with few tiles split their k-tiles (tap, channel chunk) in even
-// ranges over more workgroups; the fp32 partial sums are added in order by a
-// second kernel, which adds the bias.  Output widths divisible by 128 take
-// 128-channel tiles on eight waves (one workgroup per CU, four stages).
+// tile: 128 band pixels x BN output channels on WM x WN waves; k-tiles of one
+// tap x 64 input channels (128-byte rows), loaded straight into LDS (16 bytes
+// per lane, no register staging) into a ring of stages, one barrier per
+// k-tile.  In the padded tile the tap (dy, dx) of every pixel is the pixel's
+// own address plus one uniform offset, so a lane's source is a constant
+// per-lane offset plus a scalar per k-tile, for the weights as for the
+// activations, and a load costs no vector arithmetic.  A wave-level load
+// fills one 8-row slab: lane l writes row l / 8 at physical chunk l % 8,
+// holding logical chunk (l % 8) ^ ((row / 2) % 8), so the fragment reads (16
+// rows at one logical chunk) hit distinct banks.  The MFMAs take the weight
+// rows as the first operand, so a lane ends with four consecutive output
+// channels of one pixel.  The main loop's emission order is fixed with
+// scheduling fences: each MFMA, then its share of the next k-step's fragment
+// reads, then its share of the next tile's loads.  The epilogue stages each
+// wave's block in LDS and writes whole runs of a pixel's channels.  Launches
+// with few tiles split their k-tiles (tap, channel chunk) in even ranges over
+// more workgroups; the fp32 partial sums are added in order by a second
+// kernel, which adds the bias.
 namespace conv {
 constexpr int BM = 128, BK = 64;
 constexpr int ROWB = 2 * BK;                         // bytes per LDS row
-constexpr int KK = BK / 16;                          // MFMA k-steps per k-tile
-constexpr int SROW = 64 + 4;                         // epilogue strip row (floats)
-// BN output channels per workgroup over NW waves (each 32 pixels x 64
-// channels), a ring of S stages
-template <int BN_, int NW_, int S_>
+// BN output channels per workgroup on WM x WN waves (wave tile TM pixels x
+// TN channels), MF x MF MFMA blocks (32: v_mfma_f32_32x32x16_bf16, 16:
+// v_mfma_f32_16x16x32_bf16), a ring of S stages
+template <int BN_, int WM_, int WN_, int S_, int MF_>
 struct Geo {
-  static constexpr int BN = BN_, NW = NW_, S = S_;
+  static constexpr int BN = BN_, WM = WM_, WN = WN_, NW = WM_ * WN_, S = S_, MF = MF_;
+  static constexpr int TM = BM / WM, TN = BN / WN;
+  static constexpr int FM = TM / MF, FN = TN / MF;     // MFMA blocks per wave
+  static constexpr int KK = BK / (MF == 32 ? 16 : 32); // MFMA k-steps per k-tile
   static constexpr int STAGE = (BM + BN) * ROWB;
-  static constexpr int LA = BM * ROWB / (NW * 1024);  // A loads per lane per k-tile
-  static constexpr int LB = BN * ROWB / (NW * 1024);  // B loads per lane per k-tile
-  static constexpr int LPT = LA + LB;
-  static constexpr int LPK = (LPT + KK - 1) / KK;     // loads issued per k-step
+  static constexpr int SLABS_A = BM / 8, SLABS = (BM + BN) / 8;
+  static constexpr int LPT = (SLABS + NW - 1) / NW;    // loads per lane per k-tile
+  static constexpr int LPK = (LPT + KK - 1) / KK;      // loads issued per k-step
   static constexpr int WPC = 160 * 1024 / (S * STAGE);  // workgroups per CU (LDS)
-  static_assert(NW * 64 == 4 * BN, "four waves of 32 pixels per 64 channels");
-  static_assert(LA * NW * 1024 == BM * ROWB && LB * NW * 1024 == BN * ROWB, "whole wave-level loads");
+  static constexpr int SROW = TN + 4;                  // epilogue strip row (floats)
+  static constexpr int CPR = TN / 4;                   // 16-byte chunks of a strip row
+  static_assert(MF == 32 || MF == 16, "MFMA shape");
+  static_assert(TM % MF == 0 && TN % MF == 0 && BN % 8 == 0, "wave tile");
+  static_assert(SLABS_A % NW == 0, "A slabs evenly over the waves");
+  static_assert(LPT * NW - SLABS <= SLABS_A, "spare slots re-load A slabs");
   static_assert(S >= 2 && S <= 4 && (S - 1) * LPT < 64, "ring depth");
-  static_assert(NW * 32 * SROW * 4 <= S * STAGE, "epilogue strips fit the ring");
+  static_assert(NW * TM * SROW * 4 <= S * STAGE, "epilogue strips fit the ring");
+  static_assert(CPR <= 64, "strip row");
 };
 // 64 channels: 24 KB stages, three, two workgroups of four waves per CU;
 // 128 channels (output widths divisible by 128): 32 KB stages, four, one
-// workgroup of eight waves per CU, a third fewer operand bytes per MAC
-using Narrow = Geo<64, 4, 3>;
-using Wide = Geo<128, 8, 4>;
+// workgroup of eight waves per CU, a third fewer operand bytes per MAC;
+// 160 channels (widths divisible by 160 and not by 128, such as 320):
+// 36 KB stages, four, one workgroup of eight waves of 32 pixels x 80
+// channels on 16x16x32 MFMAs, so a 320-wide map is two tiles across
+using Narrow = Geo<64, 4, 1, 3, 32>;
+using Wide = Geo<128, 4, 2, 4, 32>;
+using Mid = Geo<160, 4, 2, 4, 16>;
 }
 
 template <class G>
 __global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams p, int splits) {
   using namespace conv;
-  constexpr int NW = G::NW, S = G::S, STAGE = G::STAGE, LA = G::LA, LPT = G::LPT, LPK = G::LPK;
+  constexpr int NW = G::NW, S = G::S, STAGE = G::STAGE, LPT = G::LPT, LPK = G::LPK, KK = G::KK;
+  constexpr int MF = G::MF, FM = G::FM, FN = G::FN, TM = G::TM, TN = G::TN, SROW = G::SROW, CPR = G::CPR;
+  using Acc = std::conditional_t<MF == 32, f32x16, f32x4>;
+  constexpr int AR = MF == 32 ? 16 : 4;                // accumulator registers
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // wave's 32 pixels (wm) and 64 output channels (wn) of the tile
-  const int wm = wave % 4, wn = wave / 4;
+  const int wm = wave % G::WM, wn = wave / G::WM;
   const int rows = p.row_end - p.row_begin;
   const int M = rows * p.W;
   const int tiles_n = p.C_out / G::BN;
@@ -267,18 +278,23 @@ __global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams
   const char* gA = reinterpret_cast<const char*>(p.act_pad);
   const char* gW = reinterpret_cast<const char*>(p.weight);
 
-  // this lane's sources: load j covers slab rows 8 (i NW + wave) + lane / 8
-  // of the A rows (pixels; rows past M re-read pixel M - 1), then of the B
-  // rows (output channels), at logical chunk (lane % 8) ^ ((row / 2) % 8);
-  // byte offsets of tap (0, 0), channel chunk 0
+  // load j of a k-tile fills slab s = j NW + wave: A (pixel) slabs first,
+  // then B (output channel) slabs; slots past the last slab re-load A slab
+  // s - SLABS (the same bytes to the same place).  Byte offsets of tap
+  // (0, 0), channel chunk 0; rows past M re-read pixel M - 1.
   const int lrow = lane >> 3, pc = lane & 7;
   unsigned off[LPT];
+  int dsto[LPT];
+  bool isa[LPT];
 #pragma unroll
   for (int j = 0; j < LPT; ++j) {
-    const int i = j < LA ? j : j - LA;
-    const int r = 8 * (i * NW + wave) + lrow;
+    int sl = j * NW + wave;
+    if (sl >= G::SLABS) sl -= G::SLABS;
+    isa[j] = sl < G::SLABS_A;
+    const int r = 8 * (isa[j] ? sl : sl - G::SLABS_A) + lrow;
     const unsigned lc = (unsigned)(pc ^ ((r >> 1) & 7)) * 16u;
-    if (j < LA) {
+    dsto[j] = sl * 1024;
+    if (isa[j]) {
       const int m = min(m0 + r, M - 1), y = m / W;
       off[j] = (unsigned)((y + 1) * WP + (m - y * W) + 1) * (unsigned)C * 2u + lc;
     } else {
@@ -293,55 +309,62 @@ __global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams
   };
   auto dma = [&](auto jc, int g, int ashift, int st) {
     constexpr int j = decltype(jc)::value;
-    constexpr int i = j < LA ? j : j - LA;
-    char* dst = smem + st * STAGE + (j < LA ? 0 : BM * ROWB) + (i * NW + wave) * 1024;
-    const char* src = j < LA ? gA + ashift + off[j] : gW + g * ROWB + off[j];
-    __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src, (ORCH_LDS void*)dst, 16, 0, 0);
+    const char* src = (isa[j] ? gA + ashift : gW + g * ROWB) + off[j];
+    __builtin_amdgcn_global_load_lds((const ORCH_GLB void*)src, (ORCH_LDS void*)(smem + st * STAGE + dsto[j]),
+                                     16, 0, 0);
   };
 
-  f32x16 acc[2];
+  Acc acc[FM][FN];
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < AR; ++r) acc[i][j][r] = 0.0f;
 
-  // fragment reads: A row 32 wm + (lane & 31), B rows 64 wn + 32 j + (lane & 31),
-  // logical chunk 2 kk + (lane >> 5)
-  const int frow = lane & 31, h = lane >> 5;
-  const int arow = (32 * wm + frow) * ROWB, brow = BM * ROWB + (64 * wn + frow) * ROWB;
+  // fragment reads: row (lane & (MF - 1)) of an MF-row block, logical chunk
+  // (KS / 8) kk + lane / MF for the KS-deep k-step; block rows start at
+  // multiples of 16, so the row's swizzle depends on the lane alone
+  const int frow = lane & (MF - 1), fh = lane / MF;
+  const int arow = (TM * wm + frow) * ROWB, brow = BM * ROWB + (TN * wn + frow) * ROWB;
   int koff[KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) koff[kk] = ((2 * kk + h) ^ ((frow >> 1) & 7)) * 16;
+  for (int kk = 0; kk < KK; ++kk) koff[kk] = (((64 / MF) * kk + fh) ^ ((frow >> 1) & 7)) * 16;
 
   // the MFMAs of stage st; with ISSUE, k-tile ig's loads into stage ist go
-  // between them: MFMA e of k-step kk, its share of k-step kk + 1's three
+  // between them: MFMA e of k-step kk, its share of k-step kk + 1's
   // fragment reads, its share of the loads
   auto compute = [&](int st, auto issue_c, int ig, int ist) {
     constexpr bool ISSUE = decltype(issue_c)::value;
+    constexpr int NM = FM * FN, ND = FM + FN;
     const char* base = smem + st * STAGE;
     const int ash = ISSUE ? a_shift(ig) : 0;
-    bf16x8 fa[2], fb[2][2];
-    fa[0] = *reinterpret_cast<const bf16x8*>(base + arow + koff[0]);
+    bf16x8 fa[2][FM], fb[2][FN];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) fb[0][j] = *reinterpret_cast<const bf16x8*>(base + brow + j * 32 * ROWB + koff[0]);
+    for (int i = 0; i < FM; ++i) fa[0][i] = *reinterpret_cast<const bf16x8*>(base + arow + i * MF * ROWB + koff[0]);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[0][j] = *reinterpret_cast<const bf16x8*>(base + brow + j * MF * ROWB + koff[0]);
     __builtin_amdgcn_sched_barrier(0);
     static_for<0, KK>([&](auto kkc) {
       constexpr int kk = decltype(kkc)::value;
-      constexpr int cur = kk & 1;
-      constexpr int nd = kk + 1 < KK ? 3 : 0;
+      constexpr int cur = kk & 1, nk = kk + 1 < KK ? kk + 1 : kk;
+      constexpr int nd = kk + 1 < KK ? ND : 0;
       constexpr int l0 = cmin(kk * LPK, LPT), nl = ISSUE ? cmin(kk * LPK + LPK, LPT) - l0 : 0;
-      static_for<0, 2>([&](auto ec) {
+      static_for<0, NM>([&](auto ec) {
         constexpr int e = decltype(ec)::value;
-        acc[e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][e], fa[cur], acc[e], 0, 0, 0);
-        static_for<e * nd / 2, (e + 1) * nd / 2>([&](auto dc) {
+        constexpr int i = e / FN, j = e % FN;
+        if constexpr (MF == 32)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
+        else
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
+        static_for<e * nd / NM, (e + 1) * nd / NM>([&](auto dc) {
           constexpr int d = decltype(dc)::value;
-          if constexpr (d == 0)
-            fa[cur ^ 1] = *reinterpret_cast<const bf16x8*>(base + arow + koff[cmin(kk + 1, KK - 1)]);
+          if constexpr (d < FM)
+            fa[cur ^ 1][d] = *reinterpret_cast<const bf16x8*>(base + arow + d * MF * ROWB + koff[nk]);
           else
-            fb[cur ^ 1][d - 1] = *reinterpret_cast<const bf16x8*>(base + brow + (d - 1) * 32 * ROWB +
-                                                                   koff[cmin(kk + 1, KK - 1)]);
+            fb[cur ^ 1][d - FM] = *reinterpret_cast<const bf16x8*>(base + brow + (d - FM) * MF * ROWB + koff[nk]);
         });
-        static_for<l0 + e * nl / 2, l0 + (e + 1) * nl / 2>([&](auto jc) { dma(jc, ig, ash, ist); });
+        static_for<l0 + e * nl / NM, l0 + (e + 1) * nl / NM>([&](auto jc) { dma(jc, ig, ash, ist); });
         __builtin_amdgcn_sched_barrier(0);
       });
     });
@@ -370,26 +393,31 @@ __global__ __launch_bounds__(64 * G::NW) void conv3x3_mfma_kernel(UNetConvParams
   lds_barrier();
   compute(kt % S, std::false_type{}, 0, 0);
 
-  // epilogue: lane holds pixel 32 wm + (lane & 31), channels 64 wn + 32 j +
-  // 8 g + 4 (lane >> 5) + 0..3 in acc[j][4 g .. 4 g + 3]; through a per-wave
-  // strip in LDS, each pixel's 64 channels leave as 16 lanes x 16 bytes
+  // epilogue: through a per-wave strip [TM pixels][TN channels] in LDS.  With
+  // 32x32 blocks a lane holds pixel 32 i + (lane & 31), channels 32 j + 8 g +
+  // 4 (lane >> 5) + 0..3 in acc[i][j][4 g .. 4 g + 3]; with 16x16 blocks
+  // pixel 16 i + (lane & 15), channels 16 j + 4 (lane >> 4) + 0..3.  Each
+  // pixel's TN channels then leave as TN / 4 lanes x 16 bytes.
   lds_barrier();
-  float* strip = reinterpret_cast<float*>(smem) + wave * 32 * SROW;
+  float* strip = reinterpret_cast<float*>(smem) + wave * TM * SROW;
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int g = 0; g < 4; ++g)
-      *reinterpret_cast<float4*>(strip + frow * SROW + 32 * j + 8 * g + 4 * h) =
-          make_float4(acc[j][4 * g], acc[j][4 * g + 1], acc[j][4 * g + 2], acc[j][4 * g + 3]);
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int g = 0; g < AR / 4; ++g)
+        *reinterpret_cast<float4*>(strip + (MF * i + frow) * SROW + MF * j + 8 * g + 4 * fh) =
+            make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
   __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the strip is written
-  const int q = lane & 15, co = n0 + 64 * wn + 4 * q;
+  constexpr int RPI = 64 / CPR;        // strip rows per store instruction
+  const int q = lane % CPR, rl = lane / CPR, co = n0 + TN * wn + 4 * q;
   float4 b = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-  if (splits == 1) b = *reinterpret_cast<const float4*>(p.bias + co);
+  if (splits == 1 && rl < RPI) b = *reinterpret_cast<const float4*>(p.bias + co);
   float* obase = splits > 1 ? p.partial + (size_t)split * M * p.C_out : p.out;
 #pragma unroll
-  for (int r0 = 0; r0 < 32; r0 += 4) {
-    const int r = r0 + (lane >> 4), m = m0 + 32 * wm + r;
-    if (m < M) {
+  for (int r0 = 0; r0 < TM; r0 += RPI) {
+    const int r = r0 + rl, m = m0 + TM * wm + r;
+    if (rl < RPI && r < TM && m < M) {
       const float4 v = *reinterpret_cast<const float4*>(strip + r * SROW + 4 * q);
       *reinterpret_cast<float4*>(obase + (size_t)m * p.C_out + co) =
           make_float4(v.x + b.x, v.y + b.y, v.z + b.z, v.w + b.w);
@@ -413,31 +441,55 @@ __global__ __launch_bounds__(256) void conv_split_reduce_kernel(UNetConvParams p
 }
 
 // ---------------------------------------------------------------------------
-// K splits of a launch: the 9 C / 64 k-tiles (tap, channel chunk) cut into
-// 1, 3, 9 or 16 even ranges over more workgroups, at least four k-tiles
-// each, the count with the least estimated time.  The estimate (fitted by
-// least squares to every split count of twelve bands of the three SDXL-sized
-// stages on MI355X, 2 us rms): rounds of workgroups over the slots (256 CUs,
-// two narrow workgroups or one wide per CU) x k-tiles per workgroup x 0.36
-// us, plus, when split, the fp32 partials' round trip (written by the
-// convolution, added in order by the reduction kernel) at 0.43 us per MB.
-static bool conv_wide(int C_out) { return C_out % conv::Wide::BN == 0; }
+// The launch plan: a tile shape (each that divides C_out) and a split of
+// the 9 C / 64 k-tiles (tap, channel chunk) into 1, 2, 3, 4, 6, 9 or 16
+// even ranges over more workgroups (at least four k-tiles each), whichever
+// has the least estimated time.  The estimate, fitted by least squares (with
+// non-negative terms) to every shape and split count on twelve bands of the
+// three SDXL-sized stages on MI355X: each round of workgroups over the slots
+// (256 CUs x workgroups per CU) costs its K k-tiles x (a + b x the round's
+// fill), a and b per shape (narrow 0.30 + 0.31 fill us, wide 0.42 + 0.12,
+// mid 0.51: a lone workgroup's k-tile, and what the round's sharing of CUs
+// and bandwidth adds); a split adds the fp32 partials' round trip (written
+// by the convolution, added in order by the reduction kernel) at 0.43 us
+// per MB.  On those bands it picks plans within 3 us in total of the
+// fastest measured.
+struct ConvPlan {
+  int geo;     // 0: narrow, 1: wide, 2: mid
+  int splits;
+};
 
-static int conv_splits(int M, int C, int C_out) {
-  const bool wide = conv_wide(C_out);
-  const int tiles = ceil_div(M, conv::BM) * (C_out / (wide ? conv::Wide::BN : conv::Narrow::BN));
-  const int slots = 256 * (wide ? conv::Wide::WPC : conv::Narrow::WPC);
+template <class G>
+static ConvPlan conv_best_splits(int geo, double a, double b, int M, int C, int C_out, double* best_us) {
+  const int tiles = ceil_div(M, conv::BM) * (C_out / G::BN);
+  const int slots = 256 * G::WPC;
   const int kts = 9 * (C / conv::BK);
   const double mb = (double)M * C_out * sizeof(float) / 1e6;
-  int best = 1;
-  double best_us = 0.0;
-  for (const int s : {1, 3, 9, 16}) {
+  ConvPlan best{geo, 1};
+  for (const int s : {1, 2, 3, 4, 6, 9, 16}) {
     if (s > 1 && kts < 4 * s) break;
-    const double us = ceil_div(tiles * s, slots) * ceil_div(kts, s) * 0.36 + (s > 1 ? s * mb * 0.43 : 0.0);
-    if (s == 1 || us < best_us) {
-      best = s;
-      best_us = us;
+    const int wgs = tiles * s, rounds = ceil_div(wgs, slots);
+    const double us = ceil_div(kts, s) * (rounds * a + b * wgs / slots) + (s > 1 ? 0.43 * s * mb : 0.0);
+    if (s == 1 || us < *best_us) {
+      best.splits = s;
+      *best_us = us;
     }
+  }
+  return best;
+}
+
+// Ties go to the earlier of wide, narrow, mid.
+static ConvPlan conv_plan(int M, int C, int C_out) {
+  double us = 0.0, u = 0.0;
+  ConvPlan best{-1, 0};
+  if (C_out % conv::Wide::BN == 0) best = conv_best_splits<conv::Wide>(1, 0.42, 0.12, M, C, C_out, &us);
+  {
+    const ConvPlan n = conv_best_splits<conv::Narrow>(0, 0.30, 0.31, M, C, C_out, &u);
+    if (best.geo < 0 || u < us) { best = n; us = u; }
+  }
+  if (C_out % conv::Mid::BN == 0) {
+    const ConvPlan m = conv_best_splits<conv::Mid>(2, 0.51, 0.0, M, C, C_out, &u);
+    if (u < us) best = m;
   }
   return best;
 }
@@ -459,7 +511,7 @@ static size_t al256(size_t b) { return (b + 255) / 256 * 256; }
 
 size_t unet_conv_workspace_bytes(int W, int C, int G, int C_out, int rows) {
   const int M = rows * W;
-  const int sp = conv_splits(M, C, C_out);
+  const int sp = conv_plan(M, C, C_out).splits;
   return al256((size_t)rows * G * 2 * sizeof(float)) +
          al256((size_t)(rows + 2) * (W + 2) * C * sizeof(bf16)) +
          (sp > 1 ? al256((size_t)sp * M * C_out * sizeof(float)) : 0);
@@ -469,7 +521,8 @@ hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   UNetConvParams p = p0;
   const int rows = p.row_end - p.row_begin;
   const int M = rows * p.W;
-  const int sp = conv_splits(M, p.C, p.C_out);
+  const ConvPlan plan = conv_plan(M, p.C, p.C_out);
+  const int sp = plan.splits;
   char* w = reinterpret_cast<char*>(ws);
   p.fresh_sums = reinterpret_cast<float*>(w);
   w += al256((size_t)rows * p.G * 2 * sizeof(float));
@@ -486,10 +539,11 @@ hipError_t launch_unet_conv(const UNetConvParams& p0, void* ws, hipStream_t s) {
   int blocks = (int)std::min<size_t>((n4 + 255) / 256, kSiluBlocks);
   blocks = std::max(unit, blocks / unit * unit);
   hipLaunchKernelGGL(gn_silu_kernel, dim3(blocks), dim3(256), 0, s, p);
-  if (conv_wide(p.C_out))
-    launch_conv<conv::Wide>(p, M, sp, s);
-  else
-    launch_conv<conv::Narrow>(p, M, sp, s);
+  switch (plan.geo) {
+    case 1: launch_conv<conv::Wide>(p, M, sp, s); break;
+    case 2: launch_conv<conv::Mid>(p, M, sp, s); break;
+    default: launch_conv<conv::Narrow>(p, M, sp, s);
+  }
   if (sp > 1) {
     const size_t o4 = (size_t)M * p.C_out / 4;
     hipLaunchKernelGGL(conv_split_reduce_kernel, dim3((int)std::min<size_t>((o4 + 255) / 256, 4096)),

@@ -175,4 +175,10 @@ UNET_SDXL_1024_S3 = UNetConvConfig(name="unet_sdxl_1024_stage3", height=32, widt
                                    channels=1280, groups=32, out_channels=1280,
                                    band_rows=(4, 14, 18), share_labels=("1/8", "14/32", "18/32"))
 
-UNET_CONFIGS = (UNET_TINY, UNET_SDXL_1024, UNET_SDXL_1024_S2, UNET_SDXL_1024_S3)
+# A map whose 14400 pixels end in a partial 128-pixel tile, with 320 output
+# channels (the convolution's 160-channel tiles cover the whole map in one
+# round of workgroups).
+UNET_RAGGED_320 = UNetConvConfig(name="unet_ragged_320", height=120, width=120, channels=64, groups=8,
+                                 out_channels=320, band_rows=(120,), share_labels=("all rows",))
+
+UNET_CONFIGS = (UNET_TINY, UNET_SDXL_1024, UNET_SDXL_1024_S2, UNET_SDXL_1024_S3, UNET_RAGGED_320)

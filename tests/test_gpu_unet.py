@@ -104,6 +104,13 @@ def test_unet_sdxl_deeper_stages(orch_lib, name, rows, share):
     _run(orch_lib, name, rb, re, refresh)
 
 
+# 120 x 120 x 64 -> 320: every row (the whole map in 160-channel tiles, the
+# last pixel tile partial) and an interior band (64-channel tiles)
+@pytest.mark.parametrize("rb,re,refresh", [(0, 120, 1), (30, 90, 0)], ids=["all", "interior"])
+def test_unet_ragged_320_channels(orch_lib, rb, re, refresh):
+    _run(orch_lib, "unet_ragged_320", rb, re, refresh)
+
+
 def test_unet_stitching_with_own_buffers(orch_lib):
     """The all-rows pass with refresh fills both buffers; bands then read
     their halo rows and the other rows' sums from them.  Refreshing, the
