@@ -166,7 +166,8 @@ def pmc_report(fetch_dir: str, write_dir: str, kernel: str = "attention") -> int
     for k in names:
         print(f"Per `{k}` dispatch (median of {len(fetch[k])} / {len(write[k])}): FETCH_SIZE "
               f"{med(fetch[k]):.1f} KiB, WRITE_SIZE {med(write[k]):.1f} KiB.\n")
-    print(f"A launch of the {kernel} is one dispatch of each; its bytes are their sum.\n")
+    print(f"A launch of the {kernel} is one dispatch of each kernel listed (the merge kernel runs only "
+          f"where query tiles are cut between workgroups); its bytes are their sum.\n")
     print(f"- kernel: {kernel}")
     print(f"- source_sha256: {kernel_source_hash(kernel)}")
     print(f"- fetch_bytes_per_launch: {fb:.0f}")

@@ -771,8 +771,13 @@ static hipError_t launch_simt(const AttnParams& p, hipStream_t s) {
 // tiles per workgroup leave CUs idle when the tile count is not close to a
 // multiple of 512 (two workgroups per CU); with a workspace, every workgroup
 // takes per = ceil(units / 512) units instead, cutting query tiles between
-// workgroups, when that shortens the longest workgroup by more than 10% (the
-// cut tiles pay for their parts and the merge).
+// workgroups, when that shortens the longest workgroup by more than
+// kCutTiles key tiles: a workgroup whose range crosses a tile boundary
+// starts a second segment (its queries and first key tiles loaded again),
+// and the parts go through the merge kernel, together about 15 us on
+// MI355X at 1.2 us a key tile.  (At DiT-XL/2 1024px, 40% band, 52 key tiles
+// per workgroup cut against 64 whole measured 77.0 against 75.3 us in the
+// step; at 25% and 65% the cut saves 9 and 22 us.)
 struct AttnPlan {
   int per, workers;
   size_t ws_bytes;   // parts of cut tiles; 0 when tiles stay whole
@@ -785,7 +790,8 @@ static AttnPlan plan_attention(int B, int heads, int n_q, int n_kv, int d) {
   const long long units = (long long)tiles * nkt;
   const int per = (int)((units + kSlots - 1) / kSlots);
   const long long whole_longest = (long long)nkt * ceil_div(tiles, kSlots);
-  if (per % nkt == 0 || (long long)per * 10 >= whole_longest * 9) return {nkt, tiles, 0};
+  constexpr int kCutTiles = 12;
+  if (per % nkt == 0 || per + kCutTiles >= whole_longest) return {nkt, tiles, 0};
   const int workers = (int)((units + per - 1) / per);
   const size_t parts = (size_t)2 * workers * mfma_attn::BQ;
   return {per, workers, (parts * d * 2 + 255) / 256 * 256 + parts * sizeof(float2)};

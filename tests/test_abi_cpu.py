@@ -125,15 +125,20 @@ def test_library_plan_rejects_bad_arguments(orch_lib, args, word):
 
 
 @pytest.mark.parametrize("n_q,n_kv,d,want", [
-    # DiT-XL/2 1024px, 40% band: 416 query tiles of 64 key tiles on 512
-    # workgroups -> 52 units each, every tile cut: 2 * 512 * 128 parts of
+    # DiT-XL/2 1024px, 25% band: 256 query tiles of 64 key tiles on 512
+    # workgroups -> 32 units each, every tile cut: 2 * 512 * 128 parts of
     # 72 bf16 + (max, sum)
-    (1664, 4096, 72, 2 * 512 * 128 * (72 * 2 + 8)),
+    (1024, 4096, 72, 2 * 512 * 128 * (72 * 2 + 8)),
+    # 20-row band: 320 tiles -> 40 units each (512 workgroups)
+    (1280, 4096, 72, 2 * 512 * 128 * (72 * 2 + 8)),
+    # 65% band: 672 tiles (two rounds of whole tiles) -> 84 units each
+    (2688, 4096, 72, 2 * 512 * 128 * (72 * 2 + 8)),
+    (1664, 4096, 72, 0),          # 40% band: 52 units cut against 64 whole, under 12 saved
     (2048, 4096, 72, 0),          # 512 tiles: one whole tile per workgroup
     (4096, 4096, 72, 0),          # 1024 tiles: two whole tiles per workgroup
-    (1664, 4096, 80, 0),          # no MFMA path for d = 80
-    (1664, 4100, 72, 0),          # keys not a multiple of 64
-    (1920, 4096, 72, 0),          # 480 tiles: cutting saves under 10%
+    (1280, 4096, 80, 0),          # no MFMA path for d = 80
+    (1280, 4100, 72, 0),          # keys not a multiple of 64
+    (1920, 4096, 72, 0),          # 480 tiles: 60 units cut against 64 whole
 ])
 def test_attention_work_plan_workspace(orch_lib, n_q, n_kv, d, want):
     """Host-side work plan of the attention: when query tiles are cut between

@@ -285,7 +285,7 @@ def test_attention(orch_lib, dtype, heads, d, n_q, n_kv, fb, nf):
 @pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("d,n_q,n_kv,fb,nf", [
     (72, 384, 4096, 1920, 384), (72, 96, 1024, 512, 96), (72, 384, 1024, 0, 0),
-    (72, 200, 1024, 64, 200), (64, 1664, 2304, 256, 1664), (72, 3328, 4096, 2048, 2048)])
+    (72, 200, 1024, 64, 200), (64, 1280, 2304, 256, 1280), (72, 3328, 4096, 2048, 2048)])
 def test_attention_split_keys(orch_lib, split, d, n_q, n_kv, fb, nf):
     """With a workspace, query tiles are cut between workgroups (parts of a
     tile from 1 to 8 workgroups, merged by a second kernel); without one,
@@ -297,8 +297,8 @@ def test_attention_split_keys(orch_lib, split, d, n_q, n_kv, fb, nf):
 
 
 @pytest.mark.parametrize("split", [False, True])
-@pytest.mark.parametrize("d,n_q,n_kv,fb,nf", [(72, 384, 1024, 256, 384), (64, 1664, 2304, 256, 1664),
-                                             (72, 1664, 4096, 0, 1664)])
+@pytest.mark.parametrize("d,n_q,n_kv,fb,nf", [(72, 384, 1024, 256, 384), (64, 1280, 2304, 256, 1280),
+                                             (72, 1280, 4096, 0, 1280), (72, 1664, 4096, 0, 1664)])
 @pytest.mark.parametrize("k_ramp,shift,k_spike", [(12.0, 0.0, 0.0), (0.0, 48.0, 0.0), (12.0, 48.0, 0.0),
                                                   (0.0, 0.0, 64.0)])
 def test_attention_running_max(orch_lib, split, d, n_q, n_kv, fb, nf, k_ramp, shift, k_spike):

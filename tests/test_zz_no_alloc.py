@@ -48,8 +48,8 @@ def _case(orch_lib, n_q, fresh_begin, seed):
 
 
 def test_no_alloc_attention_matches_workspace_entry_point(orch_lib):
-    print("\n[no-alloc attention: 1664 queries, then 384]", flush=True)
-    _case(orch_lib, 1664, 19 * 64, 0)     # 26-row band of a 64-row grid
+    print("\n[no-alloc attention: 1280 queries, then 384]", flush=True)
+    _case(orch_lib, 1280, 22 * 64, 0)     # 20-row band of a 64-row grid
     _case(orch_lib, 384, 0, 1)            # 6-row band: smaller, reuses the scratch
 
 
