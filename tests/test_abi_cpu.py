@@ -187,3 +187,42 @@ def test_library_speeds_reject(orch_lib, profs, ref, word):
     with pytest.raises(orch_lib.OrchError) as e:
         orch_lib.speeds_from_profiles(profs, ref)
     assert e.value.code == orch_lib.ORCH_EINVAL and word in orch_lib.last_error()
+
+
+def _al256(b):
+    return (b + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("H,C,Co,rows,splits", [
+    # SDXL-sized stages at 1024px (32 groups): the k-split the launch plan
+    # picks per band height (its tile shape is not visible here); the fp32
+    # partials of a split take splits x M x C_out x 4 bytes of the workspace
+    (128, 320, 320, 16, 3), (128, 320, 320, 56, 2), (128, 320, 320, 72, 1), (128, 320, 320, 128, 1),
+    (64, 640, 640, 8, 6), (64, 640, 640, 28, 4), (64, 640, 640, 36, 3), (64, 640, 640, 64, 2),
+    (32, 1280, 1280, 4, 16), (32, 1280, 1280, 14, 6), (32, 1280, 1280, 18, 6), (32, 1280, 1280, 32, 4),
+])
+def test_unet_workspace_follows_launch_plan(orch_lib, H, C, Co, rows, splits):
+    """Workspace of the U-Net band block: the band's per-row sums, the
+    zero-bordered activation tile [rows + 2][W + 2][C] bf16, and the k-split's
+    partial sums; pins the split counts the launch plan chooses."""
+    shape = orch_lib.UNetConvShape(H, H, C, 32, Co, 1e-5)
+    M = rows * H
+    want = _al256(rows * 32 * 8) + _al256((rows + 2) * (H + 2) * C * 2)
+    if splits > 1:
+        want += _al256(splits * M * Co * 4)
+    assert orch_lib.unet_conv_workspace_bytes(shape, rows) == want
+
+
+def test_unet_rejects_map_beyond_32_bit_offsets(orch_lib):
+    """The convolution indexes the activation tile and the weights with 32-bit
+    byte offsets; a map whose bf16 tile would reach 2 GiB is refused before
+    any launch."""
+    import ctypes as C
+    shape = orch_lib.UNetConvShape(4096, 4094, 64, 8, 64, 1e-5)   # 4098 x 4096 x 64 x 2 B = 2 GiB
+    rc = orch_lib.lib.orch_unet_conv_band(C.byref(shape), 0, 4, None, None, None, None, None, None, None,
+                                          0, None, None, C.c_size_t(0), None)
+    assert rc == orch_lib.ORCH_EINVAL and "too large" in orch_lib.last_error()
+    ok = orch_lib.UNetConvShape(128, 128, 320, 32, 320, 1e-5)
+    rc = orch_lib.lib.orch_unet_conv_band(C.byref(ok), 0, 4, None, None, None, None, None, None, None,
+                                          0, None, None, C.c_size_t(0), None)
+    assert rc == orch_lib.ORCH_EINVAL and "too large" not in orch_lib.last_error()
