@@ -34,6 +34,7 @@ namespace orch {
 // are added in a fixed order (the sums are bitwise reproducible), then per
 // group.
 constexpr int kRowSumThreads = 1024;
+constexpr int kRowSumBatch = 12;
 
 __global__ __launch_bounds__(kRowSumThreads) void gn_row_sums_kernel(UNetConvParams p) {
   extern __shared__ float s_part[];          // [shares][C][2]
@@ -48,11 +49,18 @@ __global__ __launch_bounds__(kRowSumThreads) void gn_row_sums_kernel(UNetConvPar
     for (int q = Q <= kRowSumThreads ? threadIdx.x % Q : threadIdx.x; q < Q;
          q += Q <= kRowSumThreads ? Q : kRowSumThreads) {
       float s[4] = {0, 0, 0, 0}, ss[4] = {0, 0, 0, 0};
-#pragma unroll 4
-      for (int x = p0; x < W; x += per) {
-        const float4 v = row[(size_t)x * Q + q];
-        s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
-        ss[0] += v.x * v.x; ss[1] += v.y * v.y; ss[2] += v.z * v.z; ss[3] += v.w * v.w;
+      // up to kRowSumBatch pixels' loads in flight, then their sums in pixel order
+      for (int x0 = p0; x0 < W; x0 += kRowSumBatch * per) {
+        float4 v[kRowSumBatch];
+#pragma unroll
+        for (int i = 0; i < kRowSumBatch; ++i)
+          if (x0 + i * per < W) v[i] = row[(size_t)(x0 + i * per) * Q + q];
+#pragma unroll
+        for (int i = 0; i < kRowSumBatch; ++i)
+          if (x0 + i * per < W) {
+            s[0] += v[i].x; s[1] += v[i].y; s[2] += v[i].z; s[3] += v[i].w;
+            ss[0] += v[i].x * v[i].x; ss[1] += v[i].y * v[i].y; ss[2] += v[i].z * v[i].z; ss[3] += v[i].w * v[i].w;
+          }
       }
       float* dst = s_part + (size_t)p0 * 2 * C + 8 * q;
 #pragma unroll
