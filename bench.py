@@ -17,10 +17,14 @@ Prints one JSON line: algorithmic TFLOP/s of the step (value), ms per step,
 the per-kernel split measured inside the steps (HIP events around every
 launch, a second pass after the timed one) with the dominant kernel's
 roofline, the HBM-bound kernels at large shapes, the share sweep (10% to
-100% bands; --no-sweep skips it), and the CPU oracle timed on one whole 10%
-band step.  --unet, --schedule and --virtual-devices time the U-Net band
-block, a band's whole sampler schedule and Algorithm 1 over virtual devices
-instead; --pmc-probe / --pmc-report serve the HBM counter runs.
+100% bands, and three shares at 2048px; --no-sweep skips it), the CPU oracle
+timed on one whole 10% band step, and one compact figure for each adjacent
+part (--no-extras skips them): the band's whole tiered sampler schedule
+(`schedule`), Algorithm 1 over four virtual devices planned from fixed
+speeds (`virtual_devices`) and the U-Net band block on three SDXL-sized
+stages (`unet`).  --unet, --schedule and --virtual-devices print only that
+figure, timed over --steps passes; --pmc-probe / --pmc-report serve the HBM
+counter runs.
 """
 from __future__ import annotations
 
@@ -47,6 +51,8 @@ MFMA_KERNELS = ("qkv_gemm", "attention", "proj_gemm", "fc1_gemm", "fc2_gemm")
 # `bench.py --pmc-probe` (FETCH_SIZE, then WRITE_SIZE) turned into a report by
 # `bench.py --pmc-report`; valid only while the kernel's sources are unchanged.
 TRAFFIC_REPORT = os.path.join(ROOT, "profiles", "attention_xl1024_band40_traffic.md")
+# timed passes of each adjacent part's figure in the default line
+EXTRA_PASSES = 3
 KERNEL_SOURCES = {
     "attention": ["paper_2509_04719_amd/csrc/k_attention.hip", "paper_2509_04719_amd/csrc/common.h",
                   "paper_2509_04719_amd/csrc/kernels.h", "paper_2509_04719_amd/build.py"],
@@ -389,10 +395,10 @@ def cpu_baseline(cfg, blob, x, labels, stale, rb, re, t, tp):
             "ms_per_step": round(dt * 1e3, 1), **info}
 
 
-def run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q) -> int:
+def schedule_result(n_passes, cfg, ctx, x, labels, kv, rows, n_q) -> dict:
     """Every executed step of the band's sampler (tiered for configs that use
     it: Algorithm 1's reduced tier, Eq. (2)); x of the band is carried from
-    step to step and the buffer refreshed on executed steps."""
+    step to step (in place) and the buffer refreshed on executed steps."""
     import torch
 
     from paper_2509_04719_amd import schedule as psched
@@ -411,25 +417,28 @@ def run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q) -> int:
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s.record()
-    for _ in range(a.steps):
+    for _ in range(n_passes):
         sampler()
     e.record()
     torch.cuda.synchronize()
-    ms = s.elapsed_time(e) / a.steps
-    res = {"metric": "full-schedule ms of one device's band sampler", "value": round(ms, 3),
-           "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": 1,
+    ms = s.elapsed_time(e) / n_passes
+    return {"metric": "full-schedule ms of one device's band sampler", "value": round(ms, 3),
+           "unit": "ms", "n_gpus": 1, "steps": n_passes, "warmup": 1,
            "ms_per_step": round(ms / len(steps), 4), "higher_is_better": False,
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": f"{cfg.name}: band {rows}/{cfg.R} rows, {len(steps)} executed "
                                   f"steps ({'tiered: warm-up ' + str(cfg.warmup) + ', then stride 2' if cfg.tiered else 'plain'})",
                       "executed_steps": len(steps), "n_q": n_q, "kv_len": cfg.n_kv},
            "tflops": round(total_flops / ms / 1e9, 1)}
-    print(json.dumps(res), flush=True)
+
+
+def run_schedule(a, cfg, ctx, x, labels, kv, rows, n_q) -> int:
+    print(json.dumps(schedule_result(a.steps, cfg, ctx, x, labels, kv, rows, n_q)), flush=True)
     ctx.close()
     return 0
 
 
-def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
+def virtual_devices_result(a, cfg, ctx, x, labels, n_passes) -> dict:
     """Algorithm 1 on virtual devices: the device planner (Eq. (2), Eq. (3))
     turns the device speeds into step counts and token rows, then the
     library's sampler runs every band's whole trajectory on this GPU."""
@@ -496,13 +505,13 @@ def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s.record()
-    for _ in range(a.steps):
+    for _ in range(n_passes):
         sample()
     e.record()
     torch.cuda.synchronize()
-    ms = s.elapsed_time(e) / a.steps
-    res = {"metric": "ms per image of the patch-parallel sampler on virtual devices", "value": round(ms, 2),
-           "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": 1, "higher_is_better": False,
+    ms = s.elapsed_time(e) / n_passes
+    return {"metric": "ms per image of the patch-parallel sampler on virtual devices", "value": round(ms, 2),
+           "unit": "ms", "n_gpus": 1, "steps": n_passes, "warmup": 1, "higher_is_better": False,
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": f"{cfg.name}: {len(tiers)} virtual devices, speeds "
                                   f"{[round(v, 4) for v in speeds]}, M_base {a.m_base}, M_warmup "
@@ -510,12 +519,15 @@ def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
                       "device_steps": steps, "device_rows": rows, "row_splits": splits,
                       "tiers": tiers, "speed_profile": profile},
            "tflops": round(flops / ms / 1e9, 1)}
-    print(json.dumps(res), flush=True)
+
+
+def run_virtual_devices(a, cfg, ctx, x, labels) -> int:
+    print(json.dumps(virtual_devices_result(a, cfg, ctx, x, labels, a.steps)), flush=True)
     ctx.close()
     return 0
 
 
-def run_unet(a) -> int:
+def unet_result(n_iters: int, with_cpu: bool) -> dict:
     """The U-Net band block (GroupNorm -> SiLU -> conv3x3 with stale halo rows
     and stale group statistics) on the three stages of an SDXL-sized U-Net at
     1024px (128 x 128 x 320, 64 x 64 x 640, 32 x 32 x 1280): ms per call and
@@ -551,7 +563,7 @@ def run_unet(a) -> int:
             xb = x[rb:re].contiguous()
             o = torch.empty((r, W, Co), device=dev)
             ms = _time_loop(torch, lambda: L.unet_conv_band(shape, rb, re, xb, gamma, beta, wt, bias,
-                                                            act, sums, 1, o, ws), a.steps)
+                                                            act, sums, 1, o, ws), n_iters)
             fl = 2.0 * r * W * Co * 9 * C
             res[f"[{rb},{re})"] = {"rows": r, "ms": round(ms, 4), "conv_tflops": round(fl / ms / 1e9, 1)}
         stages[cfg.name] = {"shape": f"{H}x{W}x{C}, {G} groups -> {Co}", "bands": res}
@@ -566,9 +578,13 @@ def run_unet(a) -> int:
                 "workload": f"{configs.UNET_SDXL_1024.name}, every row"}
     out = {"metric": "U-Net band block ms (GroupNorm, SiLU, conv3x3), SDXL-sized stages at 1024px",
            "unit": "ms", "stages": stages, "roofline": roofline}
-    if not a.no_cpu_baseline:
+    if with_cpu:
         out["cpu_baseline"] = unet_cpu_baseline(configs.UNET_SDXL_1024, 0, configs.UNET_SDXL_1024.height)
-    print(json.dumps(out), flush=True)
+    return out
+
+
+def run_unet(a) -> int:
+    print(json.dumps(unet_result(a.steps, not a.no_cpu_baseline)), flush=True)
     return 0
 
 
@@ -634,6 +650,8 @@ def main(argv=None) -> int:
     ap.add_argument("--thr-b", type=float, default=0.25)
     ap.add_argument("--unet", action="store_true",
                     help="time the U-Net band block (SDXL first stage at 1024px) instead")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the tiered-schedule, virtual-device and U-Net figures of the default line")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run the workload of the HBM counter runs and exit")
     ap.add_argument("--pmc-report", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -754,6 +772,17 @@ def main(argv=None) -> int:
         sweep2048 = sweep_2048(torch, L, a.sweep_steps)
         print(f"# sweep 2048px: {json.dumps(sweep2048)}", flush=True)
 
+    # the adjacent parts, one compact figure each (after the sweep: the
+    # schedule pass carries the band's latent forward in place)
+    extras = {}
+    if not a.no_extras:
+        extras["schedule"] = schedule_result(EXTRA_PASSES, cfg, ctx, x, labels, kv, rows, n_q)
+        print(f"# tiered schedule: {json.dumps(extras['schedule'])}", flush=True)
+        extras["virtual_devices"] = virtual_devices_result(a, cfg, ctx, x, labels, EXTRA_PASSES)
+        print(f"# virtual devices: {json.dumps(extras['virtual_devices'])}", flush=True)
+        extras["unet"] = unet_result(EXTRA_PASSES * 5, False)
+        print(f"# U-Net band block: {json.dumps(extras['unet'])}", flush=True)
+
     cpu = None
     if not a.no_cpu_baseline:
         r10 = psched.band_rows(CPU_SHARE, cfg.R)
@@ -782,6 +811,7 @@ def main(argv=None) -> int:
         "share_sweep": sweep,
         "share_sweep_2048": sweep2048,
         "cpu_baseline": cpu,
+        **extras,
     }
     print(json.dumps(res), flush=True)
     ctx.close()
