@@ -175,10 +175,11 @@ UNET_SDXL_1024_S3 = UNetConvConfig(name="unet_sdxl_1024_stage3", height=32, widt
                                    channels=1280, groups=32, out_channels=1280,
                                    band_rows=(4, 14, 18), share_labels=("1/8", "14/32", "18/32"))
 
-# A map whose 14400 pixels end in a partial 128-pixel tile, with 320 output
-# channels (the convolution's 160-channel tiles cover the whole map in one
-# round of workgroups).
-UNET_RAGGED_320 = UNetConvConfig(name="unet_ragged_320", height=120, width=120, channels=64, groups=8,
-                                 out_channels=320, band_rows=(120,), share_labels=("all rows",))
+# A map of 120 x 120 pixels (14400 in all rows, 3120 in a 26-row band: both
+# end in a partial 128-pixel tile), 192 -> 320 channels: the convolution takes
+# 160-channel tiles for all rows (one round of workgroups) and for the 26-row
+# band (its 27 k-tiles split three ways).
+UNET_RAGGED_320 = UNetConvConfig(name="unet_ragged_320", height=120, width=120, channels=192, groups=8,
+                                 out_channels=320, band_rows=(120, 26), share_labels=("all rows", "26 rows"))
 
 UNET_CONFIGS = (UNET_TINY, UNET_SDXL_1024, UNET_SDXL_1024_S2, UNET_SDXL_1024_S3, UNET_RAGGED_320)

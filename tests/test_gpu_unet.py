@@ -104,9 +104,12 @@ def test_unet_sdxl_deeper_stages(orch_lib, name, rows, share):
     _run(orch_lib, name, rb, re, refresh)
 
 
-# 120 x 120 x 64 -> 320: every row (the whole map in 160-channel tiles, the
-# last pixel tile partial) and an interior band (64-channel tiles)
-@pytest.mark.parametrize("rb,re,refresh", [(0, 120, 1), (30, 90, 0)], ids=["all", "interior"])
+# 120 x 120 x 192 -> 320: every row (the whole map in 160-channel tiles, the
+# last pixel tile partial), an interior band (64-channel tiles) and a 26-row
+# band (160-channel tiles, k-tiles split three ways, the last pixel tile
+# partial)
+@pytest.mark.parametrize("rb,re,refresh", [(0, 120, 1), (30, 90, 0), (40, 66, 1)],
+                         ids=["all", "interior", "26 rows"])
 def test_unet_ragged_320_channels(orch_lib, rb, re, refresh):
     _run(orch_lib, "unet_ragged_320", rb, re, refresh)
 
