@@ -228,7 +228,9 @@ size_t orch_unet_conv_workspace_bytes(const orch_unet_conv_shape* shape, int ban
  *   out         device fp32 [r][W][C_out].
  *   workspace   device, >= orch_unet_conv_workspace_bytes(shape, r) bytes.
  * Device pointers 16-byte aligned.  Errors: ORCH_EINVAL (shape, band, NULL
- * pointer, alignment, workspace too small), ORCH_EHIP. */
+ * pointer, alignment, workspace too small, a map of (height + 2) x (width +
+ * 2) x channels or a weight of 9 x channels x out_channels reaching 2 GiB in
+ * bf16: the kernels index them with 32-bit offsets), ORCH_EHIP. */
 int orch_unet_conv_band(const orch_unet_conv_shape* shape, int row_begin, int row_end,
                         const float* x_band, const float* gamma, const float* beta,
                         const void* weight, const float* bias, void* stale_act,
