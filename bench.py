@@ -794,7 +794,7 @@ def main(argv=None) -> int:
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: DiT-XL/2 1024px band step, {rows}/{cfg.R} token rows "
+        "config": {"workload": f"{cfg.name}: DiT-XL/2 {cfg.latent * 8}px band step, {rows}/{cfg.R} token rows "
                                f"({a.share:.0%}), {n_q} queries x {cfg.n_kv} keys, CFG batch "
                                f"{cfg.cfg_batch}, t {t}->{tp}, stale K/V refreshed",
                    "global_batch": cfg.cfg_batch, "seq_len": n_q, "kv_len": cfg.n_kv,
